@@ -1,0 +1,576 @@
+// liboptcc C ABI: argument validation, workspace carving and launch sequencing.
+//
+// Everything here runs on the host.  Arguments are checked before anything
+// is enqueued; a call either returns an error code with the device untouched
+// or enqueues its whole kernel sequence on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <type_traits>
+#include <vector>
+
+#include "optcc.h"
+#include "plan.hpp"
+#include "kernels.hpp"
+
+using namespace occ;
+
+namespace {
+
+// ----------------------------------------------------------------------------
+// optional per-kernel event timing
+// ----------------------------------------------------------------------------
+struct ProfRec {
+  const char* name;
+  hipEvent_t a, b;
+};
+
+struct Profiler {
+  bool on = false;
+  std::vector<ProfRec> recs;
+  std::vector<hipEvent_t> free_events;
+
+  hipEvent_t take() {
+    if (!free_events.empty()) {
+      hipEvent_t e = free_events.back();
+      free_events.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+};
+
+Profiler g_prof;
+
+template <typename F>
+occ_status_t launch(const char* name, hipStream_t s, F&& f) {
+  hipEvent_t a = nullptr;
+  if (g_prof.on) {
+    a = g_prof.take();
+    if (a) (void)hipEventRecord(a, s);
+  }
+  f();
+  const hipError_t e = hipGetLastError();
+  if (g_prof.on && a) {
+    hipEvent_t b = g_prof.take();
+    if (b) {
+      (void)hipEventRecord(b, s);
+      g_prof.recs.push_back({name, a, b});
+    }
+  }
+  return e == hipSuccess ? OCC_OK : OCC_E_HIP;
+}
+
+#define OCC_TRY(x)                       \
+  do {                                   \
+    const occ_status_t st_ = (x);        \
+    if (st_ != OCC_OK) return st_;       \
+  } while (0)
+
+template <typename F>
+void with_rp(int rp, F&& f) {
+  switch (rp) {
+    case 4: f(std::integral_constant<int, 4>{}); break;
+    case 8: f(std::integral_constant<int, 8>{}); break;
+    case 16: f(std::integral_constant<int, 16>{}); break;
+    case 32: f(std::integral_constant<int, 32>{}); break;
+    case 64: f(std::integral_constant<int, 64>{}); break;
+    default: f(std::integral_constant<int, 128>{}); break;
+  }
+}
+
+template <typename F>
+void with_dt_vec(int dt, bool vec, F&& f) {
+  if (dt == DT_F32) {
+    if (vec) f(std::integral_constant<int, DT_F32>{}, std::true_type{});
+    else f(std::integral_constant<int, DT_F32>{}, std::false_type{});
+  } else {
+    if (vec) f(std::integral_constant<int, DT_BF16>{}, std::true_type{});
+    else f(std::integral_constant<int, DT_BF16>{}, std::false_type{});
+  }
+}
+
+// ----------------------------------------------------------------------------
+// validation helpers
+// ----------------------------------------------------------------------------
+struct Span {
+  uintptr_t lo, hi;
+  bool writable;
+};
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+size_t elem_size(int dt) { return dt == OCC_BF16 ? 2 : 4; }
+
+Span span2d(const void* p, int64_t rows, int64_t cols, int64_t ld, size_t es, bool w) {
+  const uintptr_t lo = (uintptr_t)p;
+  return {lo, lo + (uintptr_t)(((rows - 1) * ld + cols) * (int64_t)es), w};
+}
+
+bool overlaps(std::vector<Span> v) {
+  std::sort(v.begin(), v.end(), [](const Span& a, const Span& b) { return a.lo < b.lo; });
+  // any writable interval must be disjoint from every other interval
+  for (size_t i = 0; i < v.size(); ++i) {
+    for (size_t j = i + 1; j < v.size() && v[j].lo < v[i].hi; ++j) {
+      if (v[i].writable || v[j].writable) return true;
+    }
+  }
+  return false;
+}
+
+constexpr int64_t kMaxDim = (int64_t)1 << 31;
+
+occ_status_t check_rank_iters(int rank, int iters, int64_t m, int64_t n) {
+  if (rank < 1 || rank > OCC_MAX_RANK || rank > m || rank > n) return OCC_E_RANK;
+  if (iters < 1 || iters > OCC_MAX_ITERS) return OCC_E_ITERS;
+  return OCC_OK;
+}
+
+occ_status_t check_shape(int64_t m, int64_t n, int64_t ld) {
+  if (m < 1 || n < 1 || m >= kMaxDim || n >= kMaxDim) return OCC_E_SHAPE;
+  if (ld < n || ld >= kMaxDim) return OCC_E_SHAPE;
+  if (m * ld >= ((int64_t)1 << 46)) return OCC_E_SHAPE;
+  return OCC_OK;
+}
+
+// ----------------------------------------------------------------------------
+// batch plan
+// ----------------------------------------------------------------------------
+struct Batch {
+  std::vector<Desc> descs;
+  int rp = 4, dt = 0, iters = 1;
+  bool vec = false;
+  int64_t blocks[K_NUM] = {};
+  size_t ws_needed = 0;
+};
+
+size_t table_bytes(int count) { return count > 1 ? align_up((size_t)count * sizeof(Desc)) : 0; }
+
+// Turn the workspace offsets stored in the descriptors into device addresses.
+void finalize_regions(Batch& b, void* ws) {
+  const uintptr_t base = (uintptr_t)ws;
+  for (Desc& d : b.descs) {
+    d.qpad = (float*)(base + (uintptr_t)d.qpad);
+    d.phat = (float*)(base + (uintptr_t)d.phat);
+    d.praw = (float*)(base + (uintptr_t)d.praw);
+    d.ppart = (float*)(base + (uintptr_t)d.ppart);
+    d.qpart = (float*)(base + (uintptr_t)d.qpart);
+    d.gpart = (double*)(base + (uintptr_t)d.gpart);
+    d.gsum = (double*)(base + (uintptr_t)d.gsum);
+    d.t1 = (double*)(base + (uintptr_t)d.t1);
+    d.tm = (double*)(base + (uintptr_t)d.tm);
+    d.info = (uint32_t*)(base + (uintptr_t)d.info);
+  }
+}
+
+// Validate a batch and compute its plan.  With ws == nullptr only the
+// workspace size is computed (pointers are not checked).
+occ_status_t plan_batch(const occ_mat_t* mats, int count, int rank, int iters, unsigned flags,
+                        void* ws, size_t ws_bytes, bool size_only, Batch& b) {
+  if (count < 1) return OCC_E_SHAPE;
+  if (!mats) return OCC_E_NULL;
+  if (flags & ~(unsigned)OCC_NO_MHAT) return OCC_E_FLAGS;
+  const bool write_mhat = !(flags & OCC_NO_MHAT);
+  const int dt = mats[0].m_dtype;
+  for (int j = 0; j < count; ++j) {
+    const occ_mat_t& a = mats[j];
+    if (a.m_dtype != OCC_F32 && a.m_dtype != OCC_BF16) return OCC_E_DTYPE;
+    if (a.m_dtype != dt) return OCC_E_DTYPE;
+    OCC_TRY(check_shape(a.rows, a.cols, a.ldm));
+    if (!size_only) {
+      OCC_TRY(check_shape(a.rows, a.cols, a.lde));
+      if (write_mhat) OCC_TRY(check_shape(a.rows, a.cols, a.ldh));
+    }
+    OCC_TRY(check_rank_iters(rank, iters, a.rows, a.cols));
+  }
+  b.rp = padded_rank(rank);
+  b.dt = dt;
+  b.iters = iters;
+  size_t off = kHeaderBytes + table_bytes(count);
+  b.descs.assign(count, Desc{});
+  for (int k = 0; k < K_NUM; ++k) b.blocks[k] = 0;
+  for (int j = 0; j < count; ++j) {
+    const occ_mat_t& a = mats[j];
+    const Tiling t = make_tiling(a.rows, a.cols, b.rp);
+    const Regions g = matrix_regions(a.rows, a.cols, b.rp, t);
+    Desc& d = b.descs[j];
+    d.m = (int32_t)a.rows;
+    d.n = (int32_t)a.cols;
+    d.r = rank;
+    d.n_pad = t.n_pad;
+    d.sp = t.sp;
+    d.p_cols = t.p_cols;
+    d.ng = t.ng;
+    d.sq = t.sq;
+    d.q_rows = t.q_rows;
+    for (int k = 0; k < K_NUM; ++k) {
+      d.blk[k] = (int32_t)b.blocks[k];
+      b.blocks[k] += t.blocks[k];
+      if (b.blocks[k] >= ((int64_t)1 << 31)) return OCC_E_SHAPE;
+    }
+    // remember region offsets (converted to pointers below)
+    d.qpad = (float*)(uintptr_t)(off + g.qpad);
+    d.phat = (float*)(uintptr_t)(off + g.phat);
+    d.praw = (float*)(uintptr_t)(off + g.praw);
+    d.ppart = (float*)(uintptr_t)(off + g.ppart);
+    d.qpart = (float*)(uintptr_t)(off + g.qpart);
+    d.gpart = (double*)(uintptr_t)(off + g.gpart);
+    d.gsum = (double*)(uintptr_t)(off + g.gsum);
+    d.t1 = (double*)(uintptr_t)(off + g.t1);
+    d.tm = (double*)(uintptr_t)(off + g.tm);
+    d.info = (uint32_t*)(uintptr_t)(off + g.info);
+    off += g.total;
+  }
+  b.ws_needed = off;
+  if (size_only) return OCC_OK;
+
+  // pointers, alignment, aliasing, workspace
+  if (!ws) return OCC_E_WORKSPACE;
+  bool vec = true;
+  std::vector<Span> spans;
+  for (int j = 0; j < count; ++j) {
+    const occ_mat_t& a = mats[j];
+    if (!a.M || !a.err || !a.P || !a.Q || (write_mhat && !a.M_hat)) return OCC_E_NULL;
+    const size_t es = elem_size(dt);
+    if (!aligned(a.M, es) || !aligned(a.err, 4) || !aligned(a.P, 4) || !aligned(a.Q, 4) ||
+        (write_mhat && !aligned(a.M_hat, 4)))
+      return OCC_E_ALIGN;
+    vec = vec && aligned(a.M, dt == OCC_BF16 ? 8 : 16) && a.ldm % 4 == 0 &&
+          aligned(a.err, 16) && a.lde % 4 == 0 &&
+          (!write_mhat || (aligned(a.M_hat, 16) && a.ldh % 4 == 0));
+    spans.push_back(span2d(a.M, a.rows, a.cols, a.ldm, es, false));
+    spans.push_back(span2d(a.err, a.rows, a.cols, a.lde, 4, true));
+    spans.push_back(span2d(a.P, a.rows, rank, rank, 4, true));
+    spans.push_back(span2d(a.Q, a.cols, rank, rank, 4, true));
+    if (write_mhat) spans.push_back(span2d(a.M_hat, a.rows, a.cols, a.ldh, 4, true));
+  }
+  if (!aligned(ws, kAlign)) return OCC_E_WORKSPACE;
+  if (ws_bytes < b.ws_needed) return OCC_E_WORKSPACE;
+  spans.push_back({(uintptr_t)ws, (uintptr_t)ws + b.ws_needed, true});
+  if (overlaps(spans)) return OCC_E_ALIAS;
+  b.vec = vec;
+
+  finalize_regions(b, ws);
+  for (int j = 0; j < count; ++j) {
+    const occ_mat_t& a = mats[j];
+    Desc& d = b.descs[j];
+    d.M = a.M;
+    d.err_in = a.err;
+    d.err_out = a.err;
+    d.P = a.P;
+    d.Q = a.Q;
+    d.Mhat = write_mhat ? a.M_hat : nullptr;
+    d.ldm = (int32_t)a.ldm;
+    d.lde_in = (int32_t)a.lde;
+    d.lde_out = (int32_t)a.lde;
+    d.ldh = write_mhat ? (int32_t)a.ldh : 0;
+  }
+  return OCC_OK;
+}
+
+unsigned grid_of(int64_t blocks) { return (unsigned)std::max<int64_t>(blocks, 1); }
+
+// Enqueue the compression passes (and, with `finish`, the fused
+// reconstruction/residual pass) for a planned batch.
+occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, hipStream_t s) {
+  const int count = (int)b.descs.size();
+  const Desc* table = nullptr;
+  Desc single = b.descs[0];
+  if (count > 1) {
+    Desc* dst = (Desc*)((char*)ws + kHeaderBytes);
+    table = dst;
+    for (int j0 = 0; j0 < count; j0 += kTableChunk) {
+      TableChunk c{};
+      const int nj = std::min(kTableChunk, count - j0);
+      for (int j = 0; j < nj; ++j) c.d[j] = b.descs[j0 + j];
+      OCC_TRY(launch("write_table", s, [&] {
+        hipLaunchKernelGGL(k_write_table, dim3(1), dim3(256), 0, s, dst + j0, c, nj);
+      }));
+    }
+  }
+  uint32_t* flags = (uint32_t*)ws;
+  const dim3 blk(kBlock);
+  occ_status_t st = OCC_OK;
+  with_rp(b.rp, [&](auto RPc) {
+    constexpr int RP = decltype(RPc)::value;
+    with_dt_vec(b.dt, b.vec, [&](auto DTc, auto VECc) {
+      constexpr int DT = decltype(DTc)::value;
+      constexpr bool VEC = decltype(VECc)::value;
+      auto L = [&](const char* name, auto kern, int64_t blocks, auto... extra) {
+        if (st != OCC_OK) return;
+        st = launch(name, s, [&] {
+          hipLaunchKernelGGL(kern, dim3(grid_of(blocks)), blk, 0, s, table, count, single,
+                             extra...);
+        });
+      };
+      L("qpad", k_qpad<RP>, b.blocks[K_QPAD]);
+      for (int it = 0; it < b.iters; ++it) {
+        L("pass_p", k_pass_p<DT, VEC, RP>, b.blocks[K_PASS_P]);
+        L("gram", k_gram<RP, 0>, b.blocks[K_PGRAM]);
+        L("gram_sum", k_gsum<RP, 0>, b.blocks[K_GSUM]);
+        L("chol", k_chol<RP, 0>, count, flags);
+        L("gram2", k_gram<RP, 1>, b.blocks[K_GRAM2]);
+        L("gram_sum2", k_gsum<RP, 1>, b.blocks[K_GSUM]);
+        L("chol2", k_chol<RP, 1>, count, flags);
+        L("apply", k_apply<RP>, b.blocks[K_APPLY]);
+        L("pass_q", k_pass_q<DT, VEC, RP>, b.blocks[K_PASS_Q]);
+        L("q_reduce", k_qred<RP>, b.blocks[K_QRED]);
+      }
+      if (finish) {
+        if (write_mhat)
+          L("mhat_err", k_mhat<DT, VEC, RP, 0, true, true>, b.blocks[K_MHAT]);
+        else
+          L("err_only", k_mhat<DT, VEC, RP, 0, false, true>, b.blocks[K_MHAT]);
+      }
+    });
+  });
+  return st;
+}
+
+}  // namespace
+
+// ============================================================================
+// C ABI
+// ============================================================================
+extern "C" {
+
+int occ_abi_version(void) { return OCC_ABI_VERSION; }
+
+const char* occ_status_str(int status) {
+  switch (status) {
+    case OCC_OK: return "ok";
+    case OCC_E_NULL: return "a required pointer is NULL";
+    case OCC_E_SHAPE: return "invalid shape or leading dimension";
+    case OCC_E_RANK: return "rank out of range (1 <= rank <= min(rows, cols), rank <= 128)";
+    case OCC_E_ITERS: return "iters out of range (1 <= iters <= 64)";
+    case OCC_E_DTYPE: return "unknown or mixed M dtype";
+    case OCC_E_ALIGN: return "pointer not aligned to its element size";
+    case OCC_E_ALIAS: return "buffers overlap";
+    case OCC_E_WORKSPACE: return "workspace missing, misaligned or too small";
+    case OCC_E_HIP: return "HIP runtime or kernel launch failure";
+    case OCC_E_FLAGS: return "unknown flag bit";
+    default: return "unknown status";
+  }
+}
+
+size_t occ_workspace_bytes(const occ_mat_t* mats, int count, int rank, int iters) {
+  Batch b;
+  if (plan_batch(mats, count, rank, iters, 0, nullptr, 0, true, b) != OCC_OK) return 0;
+  return b.ws_needed;
+}
+
+size_t occ_compress_workspace_bytes(int64_t m, int64_t n, int rank, int iters) {
+  occ_mat_t a{};
+  a.rows = m;
+  a.cols = n;
+  a.ldm = n;
+  a.m_dtype = OCC_F32;
+  return occ_workspace_bytes(&a, 1, rank, iters);
+}
+
+occ_status_t occ_workspace_init(void* ws, size_t ws_bytes, occ_stream_t stream) {
+  if (!ws) return OCC_E_NULL;
+  if (!aligned(ws, kAlign) || ws_bytes < kHeaderBytes) return OCC_E_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  return launch("ws_init", s, [&] {
+    hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(64), 0, s, (uint32_t*)ws,
+                       (int)(kHeaderBytes / 4));
+  });
+}
+
+occ_status_t occ_step_batched(const occ_mat_t* mats, int count, int rank, int iters,
+                              unsigned flags, void* ws, size_t ws_bytes, occ_stream_t stream) {
+  Batch b;
+  OCC_TRY(plan_batch(mats, count, rank, iters, flags, ws, ws_bytes, false, b));
+  return run_batch(b, ws, true, !(flags & OCC_NO_MHAT), (hipStream_t)stream);
+}
+
+occ_status_t occ_step(const occ_mat_t* mat, int rank, int iters, unsigned flags, void* ws,
+                      size_t ws_bytes, occ_stream_t stream) {
+  if (!mat) return OCC_E_NULL;
+  return occ_step_batched(mat, 1, rank, iters, flags, ws, ws_bytes, stream);
+}
+
+occ_status_t occ_compress(const void* M, int m_dtype, int64_t m, int64_t n, int64_t ldm,
+                          const float* err_prev, int64_t lde, float* P, float* Q, int rank,
+                          int iters, void* ws, size_t ws_bytes, occ_stream_t stream) {
+  if (m_dtype != OCC_F32 && m_dtype != OCC_BF16) return OCC_E_DTYPE;
+  OCC_TRY(check_shape(m, n, ldm));
+  if (err_prev) OCC_TRY(check_shape(m, n, lde));
+  OCC_TRY(check_rank_iters(rank, iters, m, n));
+  if (!M || !P || !Q) return OCC_E_NULL;
+  occ_mat_t a{};
+  a.M = M;
+  a.m_dtype = m_dtype;
+  a.rows = m;
+  a.cols = n;
+  a.ldm = ldm;
+  a.lde = err_prev ? lde : n;
+  a.P = P;
+  a.Q = Q;
+  Batch b;
+  OCC_TRY(plan_batch(&a, 1, rank, iters, OCC_NO_MHAT, nullptr, 0, true, b));
+  if (!ws) return OCC_E_WORKSPACE;
+  if (!aligned(ws, kAlign) || ws_bytes < b.ws_needed) return OCC_E_WORKSPACE;
+  const size_t es = elem_size(m_dtype);
+  if (!aligned(M, es) || !aligned(P, 4) || !aligned(Q, 4) || (err_prev && !aligned(err_prev, 4)))
+    return OCC_E_ALIGN;
+  std::vector<Span> spans = {span2d(M, m, n, ldm, es, false), span2d(P, m, rank, rank, 4, true),
+                             span2d(Q, n, rank, rank, 4, true),
+                             {(uintptr_t)ws, (uintptr_t)ws + b.ws_needed, true}};
+  if (err_prev) spans.push_back(span2d(err_prev, m, n, lde, 4, false));
+  if (overlaps(spans)) return OCC_E_ALIAS;
+  finalize_regions(b, ws);
+  Desc& d = b.descs[0];
+  d.M = M;
+  d.P = P;
+  d.Q = Q;
+  d.ldm = (int32_t)ldm;
+  d.err_in = err_prev;
+  d.lde_in = err_prev ? (int32_t)lde : 0;
+  d.err_out = nullptr;
+  d.Mhat = nullptr;
+  b.vec = aligned(M, m_dtype == OCC_BF16 ? 8 : 16) && ldm % 4 == 0 &&
+          (!err_prev || (aligned(err_prev, 16) && lde % 4 == 0));
+  return run_batch(b, ws, false, false, (hipStream_t)stream);
+}
+
+occ_status_t occ_decompress(const float* P, const float* Q, int64_t m, int64_t n, int rank,
+                            float* M_hat, int64_t ldh, occ_stream_t stream) {
+  OCC_TRY(check_shape(m, n, ldh));
+  if (rank < 1 || rank > OCC_MAX_RANK || rank > m || rank > n) return OCC_E_RANK;
+  if (!P || !Q || !M_hat) return OCC_E_NULL;
+  if (!aligned(P, 4) || !aligned(Q, 4) || !aligned(M_hat, 4)) return OCC_E_ALIGN;
+  std::vector<Span> spans = {span2d(P, m, rank, rank, 4, false), span2d(Q, n, rank, rank, 4, false),
+                             span2d(M_hat, m, n, ldh, 4, true)};
+  if (overlaps(spans)) return OCC_E_ALIAS;
+  const int rp = padded_rank(rank);
+  const Tiling t = make_tiling(m, n, rp);
+  Desc d{};
+  d.m = (int32_t)m;
+  d.n = (int32_t)n;
+  d.r = rank;
+  d.P = const_cast<float*>(P);
+  d.Q = const_cast<float*>(Q);
+  d.Mhat = M_hat;
+  d.ldh = (int32_t)ldh;
+  const bool vec = aligned(M_hat, 16) && ldh % 4 == 0;
+  hipStream_t s = (hipStream_t)stream;
+  occ_status_t st = OCC_OK;
+  with_rp(rp, [&](auto RPc) {
+    constexpr int RP = decltype(RPc)::value;
+    st = launch("decompress", s, [&] {
+      if (vec)
+        hipLaunchKernelGGL((k_mhat<DT_F32, true, RP, 1, true, false>),
+                           dim3(grid_of(t.blocks[K_MHAT])), dim3(kBlock), 0, s,
+                           (const Desc*)nullptr, 1, d);
+      else
+        hipLaunchKernelGGL((k_mhat<DT_F32, false, RP, 1, true, false>),
+                           dim3(grid_of(t.blocks[K_MHAT])), dim3(kBlock), 0, s,
+                           (const Desc*)nullptr, 1, d);
+    });
+  });
+  return st;
+}
+
+occ_status_t occ_err_update(const void* M, int m_dtype, int64_t m, int64_t n, int64_t ldm,
+                            const float* err_prev, int64_t lde, const float* M_hat, int64_t ldh,
+                            float* err_new, int64_t lde_new, occ_stream_t stream) {
+  if (m_dtype != OCC_F32 && m_dtype != OCC_BF16) return OCC_E_DTYPE;
+  OCC_TRY(check_shape(m, n, ldm));
+  OCC_TRY(check_shape(m, n, ldh));
+  OCC_TRY(check_shape(m, n, lde_new));
+  if (err_prev) OCC_TRY(check_shape(m, n, lde));
+  if (!M || !M_hat || !err_new) return OCC_E_NULL;
+  const size_t es = elem_size(m_dtype);
+  if (!aligned(M, es) || !aligned(M_hat, 4) || !aligned(err_new, 4) ||
+      (err_prev && !aligned(err_prev, 4)))
+    return OCC_E_ALIGN;
+  std::vector<Span> spans = {span2d(M, m, n, ldm, es, false), span2d(M_hat, m, n, ldh, 4, false),
+                             span2d(err_new, m, n, lde_new, 4, true)};
+  const bool inplace = err_prev && (const void*)err_prev == (const void*)err_new;
+  if (inplace && lde != lde_new) return OCC_E_ALIAS;
+  if (err_prev && !inplace) spans.push_back(span2d(err_prev, m, n, lde, 4, false));
+  if (overlaps(spans)) return OCC_E_ALIAS;
+  Desc d{};
+  d.M = M;
+  d.m = (int32_t)m;
+  d.n = (int32_t)n;
+  d.ldm = (int32_t)ldm;
+  d.err_in = err_prev;
+  d.lde_in = err_prev ? (int32_t)lde : 0;
+  d.Mhat = const_cast<float*>(M_hat);
+  d.ldh = (int32_t)ldh;
+  d.err_out = err_new;
+  d.lde_out = (int32_t)lde_new;
+  const int64_t total = m * n;
+  const unsigned grid = (unsigned)std::min<int64_t>((total + kBlock - 1) / kBlock, 16384);
+  hipStream_t s = (hipStream_t)stream;
+  return launch("err_update", s, [&] {
+    if (m_dtype == OCC_BF16)
+      hipLaunchKernelGGL(k_err_update<DT_BF16>, dim3(grid), dim3(kBlock), 0, s, d);
+    else
+      hipLaunchKernelGGL(k_err_update<DT_F32>, dim3(grid), dim3(kBlock), 0, s, d);
+  });
+}
+
+occ_status_t occ_get_flags(void* ws, uint32_t* flags_out, int clear, occ_stream_t stream) {
+  if (!ws || !flags_out) return OCC_E_NULL;
+  if (!aligned(ws, kAlign)) return OCC_E_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  uint32_t v = 0;
+  if (hipMemcpyAsync(&v, ws, sizeof(v), hipMemcpyDeviceToHost, s) != hipSuccess) return OCC_E_HIP;
+  if (hipStreamSynchronize(s) != hipSuccess) return OCC_E_HIP;
+  *flags_out = v;
+  if (clear) {
+    return launch("flags_clear", s, [&] {
+      hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(64), 0, s, (uint32_t*)ws, 1);
+    });
+  }
+  return OCC_OK;
+}
+
+occ_status_t occ_profile_begin(void) {
+  for (auto& r : g_prof.recs) {
+    g_prof.free_events.push_back(r.a);
+    g_prof.free_events.push_back(r.b);
+  }
+  g_prof.recs.clear();
+  g_prof.on = true;
+  return OCC_OK;
+}
+
+occ_status_t occ_profile_end(occ_kernel_time_t* out, int max, int* n_out) {
+  g_prof.on = false;
+  std::vector<occ_kernel_time_t> agg;
+  for (auto& r : g_prof.recs) {
+    if (hipEventSynchronize(r.b) != hipSuccess) return OCC_E_HIP;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) return OCC_E_HIP;
+    auto it = std::find_if(agg.begin(), agg.end(),
+                           [&](const occ_kernel_time_t& k) { return std::strcmp(k.name, r.name) == 0; });
+    if (it == agg.end()) {
+      occ_kernel_time_t k{};
+      std::snprintf(k.name, sizeof(k.name), "%s", r.name);
+      agg.push_back(k);
+      it = agg.end() - 1;
+    }
+    it->launches += 1;
+    it->total_ms += ms;
+  }
+  for (auto& r : g_prof.recs) {
+    g_prof.free_events.push_back(r.a);
+    g_prof.free_events.push_back(r.b);
+  }
+  g_prof.recs.clear();
+  if (n_out) *n_out = (int)agg.size();
+  if (out)
+    for (int i = 0; i < (int)agg.size() && i < max; ++i) out[i] = agg[i];
+  return OCC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,89 @@
+"""GPU parity: liboptcc (through its binding) against the float64 oracle.
+
+Sizes are chosen so the oracle finishes in seconds while the kernels still
+see several tiles and ragged tails; the full-size workloads are in
+test_gpu_full.py.  Tolerance (relative Frobenius error of M_hat and of err):
+1e-4 for fp32 M, 2e-2 for bf16 M (fp32 accumulation).
+"""
+
+import numpy as np
+import pytest
+
+from gpu_util import TOL, assert_parity, rel_f, run_workload, to_device, to_host, torch_mod
+from workloads import WORKLOADS, Workload, high_snr
+
+pytestmark = pytest.mark.gpu
+
+
+def test_config1_full_size():
+    res, _, _ = run_workload(WORKLOADS[1], 1)
+    assert_parity(res, "f32", "gauss_1024 r4 t1")
+
+
+def test_config2_ragged_multistep():
+    w = WORKLOADS[2].scaled([(1000, 700)])
+    res, _, _ = run_workload(w, 4)
+    assert_parity(res, "bf16", "act_grad 1000x700 r16 t1 x4 steps")
+
+
+def test_config2_high_snr_ragged():
+    w = high_snr(WORKLOADS[2].scaled([(777, 520)]))
+    res, _, _ = run_workload(w, 3)
+    assert_parity(res, "bf16", "act_grad high-SNR 777x520")
+
+
+@pytest.mark.parametrize("rank", [1, 3, 4, 8, 16, 17, 32, 64, 100, 128])
+@pytest.mark.parametrize("iters", [1, 2])
+def test_rank_sweep_fp32(rank, iters):
+    w = Workload(90, "sweep", ((300, 257),), "f32", rank, iters, 2, "gauss", std=1.0)
+    res, _, _ = run_workload(w, 2)
+    assert_parity(res, "f32", f"sweep 300x257 r{rank} t{iters}")
+
+
+@pytest.mark.parametrize("rank", [4, 16, 33, 128])
+def test_rank_sweep_bf16(rank):
+    w = WORKLOADS[2].scaled([(600, 333)], rank=rank, signal_rank=48)
+    res, _, _ = run_workload(w, 2)
+    assert_parity(res, "bf16", f"bf16 600x333 r{rank}")
+
+
+def test_config3_stage_batched_small():
+    shapes = [(3 * 96, 96), (96, 96), (4 * 96, 96), (96, 4 * 96)] * 2
+    w = WORKLOADS[3].scaled(shapes)
+    res, _, _ = run_workload(w, 2, batched=True)
+    assert_parity(res, "f32", "stage weights h=96 x2 layers, batched")
+
+
+def test_config4_zipf_small():
+    w = WORKLOADS[4].scaled([(2000, 300)], tokens=400)
+    res, _, _ = run_workload(w, 2)
+    assert_parity(res, "f32", "embedding 2000x300 zipf")
+
+
+def test_config5_batched_small():
+    w = WORKLOADS[5].scaled([(700, 520)] * 2, signal_rank=160)
+    res, _, _ = run_workload(w, 2, batched=True)
+    assert_parity(res, "bf16", "act_grad 2x700x520 r128 t2 batched")
+
+
+def test_config5_high_snr_small():
+    w = high_snr(WORKLOADS[5].scaled([(700, 520)], signal_rank=160))
+    res, _, _ = run_workload(w, 2)
+    assert_parity(res, "bf16", "act_grad high-SNR 700x520 r128 t2")
+
+
+@pytest.mark.parametrize("shape,rank", [((1, 1), 1), ((5, 3), 3), ((64, 1), 1), ((1, 100), 1),
+                                        ((65, 33), 8), ((3, 200), 2)])
+def test_tiny_shapes(shape, rank):
+    w = Workload(91, "tiny", (shape,), "f32", rank, 1, 1, "gauss", std=1.0)
+    res, _, _ = run_workload(w, 1)
+    assert_parity(res, "f32", f"tiny {shape} r{rank}")
+
+
+def test_unaligned_leading_dimension():
+    w = Workload(92, "ldpad", ((130, 75),), "f32", 8, 2, 2, "gauss", std=1.0)
+    res, _, _ = run_workload(w, 2, ld_pad=1)
+    assert_parity(res, "f32", "ld = n + 1 (scalar path)")
+    wb = WORKLOADS[2].scaled([(130, 75)], rank=8)
+    res, _, _ = run_workload(wb, 2, ld_pad=3)
+    assert_parity(res, "bf16", "bf16 ld = n + 3 (scalar path)")
