@@ -1,0 +1,289 @@
+#!/usr/bin/env python3
+"""Throughput of the fused compress + decompress + error-update step on one MI355X.
+
+Default workload: the 8192x4096 bf16 inter-stage activation gradient, rank 16,
+one power iteration, error buffer and Q carried from step to step, a fresh
+seeded input each step (8 distinct inputs, cycled).  A step is one
+occ_step call: error-feedback add, left product, CholeskyQR, right product,
+reconstruction and residual.
+
+Prints ONE JSON line.  `value` is input GB/s (bytes of M as stored, per step,
+over the measured step time) with every input already resident in HBM.
+`roofline` is measured for the kernel that takes the most time, from HIP
+events bracketing each of its launches on the library's stream, against the
+8 TB/s HBM3E peak; `traffic` comes from the committed rocprofv3 counter
+summary in profiles/ when it matches the current kernel sources.
+`cpu_baseline` times the float64 oracle on this host on a bounded sample of
+the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 1..5]
+"""
+
+from __future__ import annotations
+
+import argparse
+import glob
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "compress+decompress+err-update input GB/s and % of HBM roofline, 1 MI355X"
+HBM_PEAK_GBS = 8000.0
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = ["paper_2301_09830_amd/csrc/kernels.hpp", "paper_2301_09830_amd/csrc/plan.hpp",
+                  "paper_2301_09830_amd/csrc/api.hip"]
+
+
+def kernel_source_digest() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+# ----------------------------------------------------------------------------
+# algorithmic byte accounting (bytes that must cross HBM, per element of M)
+# ----------------------------------------------------------------------------
+def kernel_alg_bytes(kernel: str, elements: int, m_bytes: int) -> int | None:
+    """Bytes one launch of a streaming kernel must move for `elements` of M.
+
+    pass_p / pass_q read M and err once (m_bytes + 4 per element);
+    mhat_err reads M and err and writes err and M_hat (m_bytes + 12);
+    err_only reads M and err and writes err (m_bytes + 8).
+    """
+    per = {"pass_p": m_bytes + 4, "pass_q": m_bytes + 4, "mhat_err": m_bytes + 12,
+           "err_only": m_bytes + 8}.get(kernel)
+    return None if per is None else per * elements
+
+
+def step_alg_bytes(elements: int, m_bytes: int, iters: int, write_mhat: bool = True) -> int:
+    """2*iters+1 streaming passes over M and err, plus the err (and M_hat) writes."""
+    return elements * ((2 * iters + 1) * (m_bytes + 4) + 4 + (4 if write_mhat else 0))
+
+
+def load_traffic(kernel: str, workload: str, launches_elements: int):
+    """HBM bytes per launch from the committed counter summary, or None."""
+    path = os.path.join(PROFILES, f"{kernel}__{workload}__pmc.md")
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    start = text.find("```json")
+    if start < 0:
+        return None
+    end = text.find("```", start + 7)
+    try:
+        rec = json.loads(text[start + 7:end])
+    except ValueError:
+        return None
+    if rec.get("kernel_source_sha") != kernel_source_digest():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+# ----------------------------------------------------------------------------
+# workload setup
+# ----------------------------------------------------------------------------
+def gen_inputs(w, n_inputs: int):
+    """Stored-dtype host matrices: n_inputs steps x len(w.shapes) matrices."""
+    from concurrent.futures import ThreadPoolExecutor
+    jobs = [(s, j) for s in range(n_inputs) for j in range(len(w.shapes))]
+    with ThreadPoolExecutor(max_workers=min(8, len(jobs))) as ex:
+        mats = list(ex.map(lambda sj: w.matrix(*sj), jobs))
+    return {sj: m for sj, m in zip(jobs, mats)}
+
+
+def to_device(x, dtype: str):
+    import numpy as np
+    import torch
+    if dtype == "f32":
+        return torch.from_numpy(np.ascontiguousarray(x)).cuda()
+    return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def cpu_baseline(w, host, seconds: float):
+    """Time oracle.step on this host's cores over a bounded sample."""
+    import numpy as np
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
+    except Exception:
+        cores = int(os.environ.get("OMP_NUM_THREADS", "1"))
+    import oracle
+    count = len(w.shapes)
+    state = {j: (np.zeros(w.shapes[j]), w.q0(j).astype(np.float64)) for j in range(count)}
+    n_inputs = len({s for (s, _) in host})
+    done_bytes, steps, mats = 0, 0, 0
+    t0 = time.perf_counter()
+    while True:
+        s = steps % n_inputs
+        for j in range(count):
+            e, q = state[j]
+            out = oracle.step(host[(s, j)], w.m_dtype, e, q, w.rank, w.iters)
+            state[j] = (out["err"], out["Q"])
+            done_bytes += host[(s, j)].nbytes
+            mats += 1
+            if time.perf_counter() - t0 > seconds:
+                break
+        steps += 1
+        if time.perf_counter() - t0 > seconds:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": round(done_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": int(cores),
+            "kind": "oracle", "seconds": round(dt, 2),
+            "sample": f"{mats} matrix steps of {w.name} (oracle.step, float64, "
+                      f"carried err/Q) on {cores} BLAS threads"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=400)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--inputs", type=int, default=0,
+                    help="distinct seeded inputs cycled through (default: the workload's steps)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--no-kernel-timing", action="store_true")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="also run a plain device copy of this size (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print(json.dumps({"metric": METRIC, "error": "liboptcc runs on one GPU; "
+                          "multi-GPU runs are not part of this benchmark (use --gpus 1)"}))
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2301_09830_amd import optcc
+    from workloads import WORKLOADS
+
+    w = WORKLOADS[args.workload]
+    n_inputs = args.inputs or w.steps
+    host = gen_inputs(w, n_inputs)
+    count = len(w.shapes)
+    dev_M = {k: to_device(v, w.m_dtype) for k, v in host.items()}
+    errs = [torch.zeros(s, dtype=torch.float32, device="cuda") for s in w.shapes]
+    Qs = [torch.from_numpy(w.q0(j)).cuda() for j in range(count)]
+    Ps = [torch.empty((s[0], w.rank), dtype=torch.float32, device="cuda") for s in w.shapes]
+    Mhs = [torch.empty(s, dtype=torch.float32, device="cuda") for s in w.shapes]
+    L = optcc.lib()
+    arrays = []
+    for s in range(n_inputs):
+        arr = (optcc.occ_mat_t * count)()
+        for j in range(count):
+            mat = optcc.make_mat(dev_M[(s, j)], errs[j], Ps[j], Qs[j], Mhs[j])
+            arr[j] = mat
+        arrays.append(arr)
+    ws_bytes = L.occ_workspace_bytes(arrays[0], count, w.rank, w.iters)
+    ws = optcc.alloc_workspace(ws_bytes)
+    stream = torch.cuda.current_stream()
+    sptr = int(stream.cuda_stream)
+    wsp = int(ws.data_ptr())
+
+    def step(k: int) -> None:
+        st = L.occ_step_batched(arrays[k % n_inputs], count, w.rank, w.iters, 0, wsp, ws_bytes,
+                                sptr)
+        if st != 0:
+            raise optcc.OccError("occ_step_batched", st)
+
+    for k in range(args.warmup):
+        step(k)
+    torch.cuda.synchronize()
+
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for k in range(args.steps):
+        step(args.warmup + k)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_events = ev0.elapsed_time(ev1)
+    ms_per_step = ms_events / args.steps
+
+    elements = w.elements
+    m_bytes = 2 if w.m_dtype == "bf16" else 4
+    input_bytes = w.m_bytes
+    value = input_bytes / (ms_per_step * 1e-3) / 1e9
+    step_bytes = step_alg_bytes(elements, m_bytes, w.iters)
+
+    kernels = {}
+    roofline = None
+    if not args.no_kernel_timing:
+        optcc.occ_profile_begin()
+        for k in range(args.steps):
+            step(k)
+        prof = optcc.occ_profile_end()
+        for name, (launches, total_ms) in prof.items():
+            kernels[name] = {"launches_per_step": round(launches / args.steps, 3),
+                             "avg_us": round(total_ms / launches * 1e3, 3),
+                             "share": None}
+        tot = sum(v[1] for v in prof.values())
+        for name in kernels:
+            kernels[name]["share"] = round(prof[name][1] / tot, 4) if tot else None
+        streaming = {k: v for k, v in prof.items() if kernel_alg_bytes(k, 1, m_bytes)}
+        if streaming:
+            dom = max(streaming, key=lambda k: streaming[k][1])
+            launches, total_ms = prof[dom]
+            avg_s = total_ms / launches * 1e-3
+            per_launch = kernel_alg_bytes(dom, elements, m_bytes)  # one launch covers the batch
+            achieved = per_launch / avg_s / 1e9
+            traffic = load_traffic(dom, w.name, elements)
+            roofline = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1),
+                        "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": round(achieved / HBM_PEAK_GBS, 4),
+                        "traffic": traffic, "alg_bytes_per_launch": int(per_launch),
+                        "avg_launch_us": round(avg_s * 1e6, 3)}
+
+    if args.calibrate_copy_mib:
+        n = args.calibrate_copy_mib * (1 << 20) // 4
+        a = torch.empty(n, dtype=torch.float32, device="cuda").normal_()
+        b = torch.empty_like(a)
+        for _ in range(5):
+            b.copy_(a)
+        torch.cuda.synchronize()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, host, args.cpu_seconds)
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "shapes": [list(s) for s in w.shapes],
+                   "m_dtype": w.m_dtype, "rank": w.rank, "iters": w.iters,
+                   "distinct_inputs": n_inputs, "state": "err and Q carried across steps"},
+        "step_roofline": {"alg_bytes_per_step": step_bytes,
+                          "achieved": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+                          "frac": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "kernels": kernels,
+        "wall_s": round(wall, 3),
+    }
+    print(json.dumps(out))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -14,6 +14,8 @@
 #include "optcc.h"
 #include "plan.hpp"
 #include "kernels.hpp"
+#include "kernels_small.hpp"
+#include "kernels_mfma16.hpp"
 
 using namespace occ;
 
@@ -144,6 +146,7 @@ struct Batch {
   std::vector<Desc> descs;
   int rp = 4, dt = 0, iters = 1;
   bool vec = false;
+  bool fused = false;
   int64_t blocks[K_NUM] = {};
   size_t ws_needed = 0;
 };
@@ -160,6 +163,7 @@ void finalize_regions(Batch& b, void* ws) {
     d.ppart = (float*)(base + (uintptr_t)d.ppart);
     d.qpart = (float*)(base + (uintptr_t)d.qpart);
     d.gpart = (double*)(base + (uintptr_t)d.gpart);
+    d.gsub = (double*)(base + (uintptr_t)d.gsub);
     d.gsum = (double*)(base + (uintptr_t)d.gsum);
     d.t1 = (double*)(base + (uintptr_t)d.t1);
     d.tm = (double*)(base + (uintptr_t)d.tm);
@@ -190,12 +194,13 @@ occ_status_t plan_batch(const occ_mat_t* mats, int count, int rank, int iters, u
   b.rp = padded_rank(rank);
   b.dt = dt;
   b.iters = iters;
+  b.fused = b.rp <= kFusedMaxRank;
   size_t off = kHeaderBytes + table_bytes(count);
   b.descs.assign(count, Desc{});
   for (int k = 0; k < K_NUM; ++k) b.blocks[k] = 0;
   for (int j = 0; j < count; ++j) {
     const occ_mat_t& a = mats[j];
-    const Tiling t = make_tiling(a.rows, a.cols, b.rp);
+    const Tiling t = make_tiling(a.rows, a.cols, b.rp, b.fused);
     const Regions g = matrix_regions(a.rows, a.cols, b.rp, t);
     Desc& d = b.descs[j];
     d.m = (int32_t)a.rows;
@@ -207,6 +212,8 @@ occ_status_t plan_batch(const occ_mat_t* mats, int count, int rank, int iters, u
     d.ng = t.ng;
     d.sq = t.sq;
     d.q_rows = t.q_rows;
+    d.gb = t.gb;
+    d.fused = b.fused ? 1 : 0;
     for (int k = 0; k < K_NUM; ++k) {
       d.blk[k] = (int32_t)b.blocks[k];
       b.blocks[k] += t.blocks[k];
@@ -219,6 +226,7 @@ occ_status_t plan_batch(const occ_mat_t* mats, int count, int rank, int iters, u
     d.ppart = (float*)(uintptr_t)(off + g.ppart);
     d.qpart = (float*)(uintptr_t)(off + g.qpart);
     d.gpart = (double*)(uintptr_t)(off + g.gpart);
+    d.gsub = (double*)(uintptr_t)(off + g.gsub);
     d.gsum = (double*)(uintptr_t)(off + g.gsum);
     d.t1 = (double*)(uintptr_t)(off + g.t1);
     d.tm = (double*)(uintptr_t)(off + g.tm);
@@ -239,7 +247,7 @@ occ_status_t plan_batch(const occ_mat_t* mats, int count, int rank, int iters, u
     if (!aligned(a.M, es) || !aligned(a.err, 4) || !aligned(a.P, 4) || !aligned(a.Q, 4) ||
         (write_mhat && !aligned(a.M_hat, 4)))
       return OCC_E_ALIGN;
-    vec = vec && aligned(a.M, dt == OCC_BF16 ? 8 : 16) && a.ldm % 4 == 0 &&
+    vec = vec && aligned(a.M, 16) && a.ldm % (dt == OCC_BF16 ? 8 : 4) == 0 &&
           aligned(a.err, 16) && a.lde % 4 == 0 &&
           (!write_mhat || (aligned(a.M_hat, 16) && a.ldh % 4 == 0));
     spans.push_back(span2d(a.M, a.rows, a.cols, a.ldm, es, false));
@@ -300,13 +308,34 @@ occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, h
     with_dt_vec(b.dt, b.vec, [&](auto DTc, auto VECc) {
       constexpr int DT = decltype(DTc)::value;
       constexpr bool VEC = decltype(VECc)::value;
-      auto L = [&](const char* name, auto kern, int64_t blocks, auto... extra) {
+      auto LB = [&](const char* name, auto kern, int64_t blocks, int threads, auto... extra) {
         if (st != OCC_OK) return;
         st = launch(name, s, [&] {
-          hipLaunchKernelGGL(kern, dim3(grid_of(blocks)), blk, 0, s, table, count, single,
-                             extra...);
+          hipLaunchKernelGGL(kern, dim3(grid_of(blocks)), dim3(threads), 0, s, table, count,
+                             single, extra...);
         });
       };
+      auto L = [&](const char* name, auto kern, int64_t blocks, auto... extra) {
+        LB(name, kern, blocks, kBlock, extra...);
+      };
+      if constexpr (RP <= kFusedMaxRank) {
+        if (b.fused) {
+          if (b.descs[0].r != RP) L("qpad", k_qpad<RP>, b.blocks[K_QPAD]);
+          for (int it = 0; it < b.iters; ++it) {
+            LB("pass_p", k_pm<DT, VEC, RP>, b.blocks[K_PASS_P], PM_THREADS);
+            LB("orth", k_orth16<RP>, b.blocks[K_PGRAM], CH_THREADS, flags);
+            L("pass_q", k_qm<DT, VEC, RP>, b.blocks[K_PASS_Q]);
+            L("q_reduce", k_qred16<RP>, b.blocks[K_QRED]);
+          }
+          if (finish) {
+            if (write_mhat)
+              L("mhat_err", k_mh16<DT, VEC, RP, true>, b.blocks[K_MHAT]);
+            else
+              L("err_only", k_mh16<DT, VEC, RP, false>, b.blocks[K_MHAT]);
+          }
+          return;
+        }
+      }
       L("qpad", k_qpad<RP>, b.blocks[K_QPAD]);
       for (int it = 0; it < b.iters; ++it) {
         L("pass_p", k_pass_p<DT, VEC, RP>, b.blocks[K_PASS_P]);
@@ -377,7 +406,7 @@ occ_status_t occ_workspace_init(void* ws, size_t ws_bytes, occ_stream_t stream) 
   if (!aligned(ws, kAlign) || ws_bytes < kHeaderBytes) return OCC_E_WORKSPACE;
   hipStream_t s = (hipStream_t)stream;
   return launch("ws_init", s, [&] {
-    hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(64), 0, s, (uint32_t*)ws,
+    hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(256), 0, s, (uint32_t*)ws,
                        (int)(kHeaderBytes / 4));
   });
 }
@@ -434,7 +463,7 @@ occ_status_t occ_compress(const void* M, int m_dtype, int64_t m, int64_t n, int6
   d.lde_in = err_prev ? (int32_t)lde : 0;
   d.err_out = nullptr;
   d.Mhat = nullptr;
-  b.vec = aligned(M, m_dtype == OCC_BF16 ? 8 : 16) && ldm % 4 == 0 &&
+  b.vec = aligned(M, 16) && ldm % (m_dtype == OCC_BF16 ? 8 : 4) == 0 &&
           (!err_prev || (aligned(err_prev, 16) && lde % 4 == 0));
   return run_batch(b, ws, false, false, (hipStream_t)stream);
 }
@@ -449,7 +478,7 @@ occ_status_t occ_decompress(const float* P, const float* Q, int64_t m, int64_t n
                              span2d(M_hat, m, n, ldh, 4, true)};
   if (overlaps(spans)) return OCC_E_ALIAS;
   const int rp = padded_rank(rank);
-  const Tiling t = make_tiling(m, n, rp);
+  const Tiling t = make_tiling(m, n, rp, false);
   Desc d{};
   d.m = (int32_t)m;
   d.n = (int32_t)n;

@@ -29,6 +29,12 @@ __device__ __forceinline__ cdouble_p as_const(const double* p) { return (cdouble
 enum { DT_F32 = 0, DT_BF16 = 1 };
 enum : uint32_t { FLAG_NONFINITE = 1u, FLAG_RANK_DEFICIENT = 2u };
 
+// Index of this thread's wave in its block, as a wave-uniform (SGPR) value so
+// that addresses derived from it qualify for scalar loads.
+__device__ __forceinline__ int wave_id() {
+  return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+}
+
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
@@ -132,7 +138,7 @@ __global__ __launch_bounds__(kBlock) void k_qpad(OCC_KARGS) {
 // ---------------------------------------------------------------------------
 template <int DT, bool VEC, int RP>
 __device__ __forceinline__ void pass_p_body(const Desc& d, int b, float* lds) {
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = wave_id(), lane = threadIdx.x & 63;
   const int row_tiles = (d.m + PP_ROWS - 1) / PP_ROWS;
   const int tile = b % row_tiles, split = b / row_tiles;
   const int row0 = tile * PP_ROWS;
@@ -539,7 +545,7 @@ __device__ __forceinline__ void pass_q_body(const Desc& d, int b, float* lds) {
   constexpr int CPL = cols_per_lane(RP);
   constexpr int RC = q_rank_chunk(RP);
   constexpr int NRC = RP / RC;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = wave_id(), lane = threadIdx.x & 63;
   const int col_tiles = (d.n + 64 * CPL - 1) / (64 * CPL);
   const int rc = b % NRC;
   const int rest = b / NRC;
@@ -630,7 +636,7 @@ __global__ __launch_bounds__(kBlock) void k_qred(OCC_KARGS) {
 template <int DT, bool VEC, int RP, int SRC, bool WRITE_MHAT, bool WRITE_ERR>
 __device__ __forceinline__ void mhat_body(const Desc& d, int b) {
   constexpr int CPL = cols_per_lane(RP);
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int wave = wave_id(), lane = threadIdx.x & 63;
   const int col_tiles = (d.n + 64 * CPL - 1) / (64 * CPL);
   const int ct = b % col_tiles, rb = b / col_tiles;
   const int c0 = ct * 64 * CPL + lane * CPL;

@@ -1,0 +1,299 @@
+// Small-rank products on the matrix cores (padded rank RP <= 16).
+//
+// Both tall-skinny products of a power-iteration round are dense
+// contractions with a 16-wide output dimension; v_mfma_f32_16x16x4_f32 takes
+// its two operands spread over the 64 lanes (one value per lane), so the
+// 16-wide factor (Q rows in the left product, P_hat rows in the right one)
+// never has to be broadcast, and A goes straight from 16-byte global loads
+// into the instruction.  Arithmetic is fp32 products with fp32 accumulation,
+// like the vector-ALU path.
+//
+// Lane layout of v_mfma_f32_16x16x4_f32 (lane l = 16*g + li):
+//   A operand  a = A[i = li][k = g]      B operand  b = B[k = g][j = li]
+//   result     D[i = 4*g + v][j = li] in component v of the float4.
+//
+//   k_pm   P = A Q.  A block owns 32 whole rows (two 16-row MFMA tiles);
+//          each wave walks 32-column K-steps: lane (g, li) loads 8
+//          consecutive columns 8g..8g+7 of row li (a full 128-byte line of err
+//          per 4 lanes) and feeds them to 8 MFMAs whose K index is column
+//          8g+j.  The B operand is Q[8g+j][li].  The next K-step's A and Q are
+//          loaded before the current one is used.
+//   k_qm   Q = A^T P_hat partials.  A block owns 128 columns and a row split;
+//          each wave takes a quarter of the rows in 4-row K-steps: lane
+//          (g, li) loads columns 8li..8li+7 of row g and feeds 8 MFMAs, MFMA t
+//          producing the interleaved column tile {8m + t}.  The B operand is
+//          P_hat[row g][li].
+#pragma once
+
+#include "kernels_small.hpp"
+
+namespace occ {
+
+typedef float f4v __attribute__((ext_vector_type(4)));
+
+constexpr int PM_RB = 2;                  // 16-row MFMA tiles per block in k_pm
+constexpr int PM_ROWS = 16 * PM_RB;       // rows per block (== F_PROWS)
+constexpr int PM_WAVES = 8;               // waves per block in k_pm
+constexpr int PM_THREADS = PM_WAVES * kWave;
+static_assert(PM_ROWS == F_PROWS, "k_pm block rows must match the plan");
+constexpr int QM_COLS = F_QCOLS;          // columns per block in k_qm
+
+__device__ __forceinline__ f4v mfma4(float a, float b, f4v c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// Eight consecutive elements of A = M + err_prev (columns c..c+7 of one row),
+// kept as raw loads until used.  Out-of-range or unaligned chunks hold the
+// exact element-wise A in e0/e1 and -0 in m (x + -0 == x for every x).
+template <int DT> struct Ch8;
+template <> struct Ch8<DT_BF16> { uint4 m; float4 e0, e1; };
+template <> struct Ch8<DT_F32> { float4 m0, m1; float4 e0, e1; };
+
+template <int DT>
+__device__ __forceinline__ void ch8_neg_zero(Ch8<DT>& x) {
+  if constexpr (DT == DT_BF16) {
+    x.m = make_uint4(0x80008000u, 0x80008000u, 0x80008000u, 0x80008000u);
+  } else {
+    x.m0 = make_float4(-0.f, -0.f, -0.f, -0.f);
+    x.m1 = x.m0;
+  }
+}
+
+template <int DT, bool VEC>
+__device__ __forceinline__ Ch8<DT> ch8_load(const Desc& d, int row, int c, int c_hi) {
+  Ch8<DT> x;
+  if (VEC && row < d.m && c + 8 <= c_hi) {
+    const int64_t mo = (int64_t)row * d.ldm + c;
+    if constexpr (DT == DT_BF16) {
+      x.m = *(const uint4*)((const uint16_t*)d.M + mo);
+    } else {
+      x.m0 = *(const float4*)((const float*)d.M + mo);
+      x.m1 = *(const float4*)((const float*)d.M + mo + 4);
+    }
+    if (d.err_in) {
+      const float* e = d.err_in + (int64_t)row * d.lde_in + c;
+      x.e0 = *(const float4*)e;
+      x.e1 = *(const float4*)(e + 4);
+    } else {
+      x.e0 = make_float4(-0.f, -0.f, -0.f, -0.f);
+      x.e1 = x.e0;
+    }
+  } else {
+    float lo[4], hi[4];
+    load_a4<DT, false>(d, row, c, c_hi, lo);
+    load_a4<DT, false>(d, row, c + 4, c_hi, hi);
+    ch8_neg_zero<DT>(x);
+    x.e0 = make_float4(lo[0], lo[1], lo[2], lo[3]);
+    x.e1 = make_float4(hi[0], hi[1], hi[2], hi[3]);
+  }
+  return x;
+}
+
+// The eight A values of a chunk.
+template <int DT>
+__device__ __forceinline__ void ch8_values(const Ch8<DT>& x, float a[8]) {
+  if constexpr (DT == DT_BF16) {
+    a[0] = bf16_lo(x.m.x) + x.e0.x; a[1] = bf16_hi(x.m.x) + x.e0.y;
+    a[2] = bf16_lo(x.m.y) + x.e0.z; a[3] = bf16_hi(x.m.y) + x.e0.w;
+    a[4] = bf16_lo(x.m.z) + x.e1.x; a[5] = bf16_hi(x.m.z) + x.e1.y;
+    a[6] = bf16_lo(x.m.w) + x.e1.z; a[7] = bf16_hi(x.m.w) + x.e1.w;
+  } else {
+    a[0] = x.m0.x + x.e0.x; a[1] = x.m0.y + x.e0.y; a[2] = x.m0.z + x.e0.z; a[3] = x.m0.w + x.e0.w;
+    a[4] = x.m1.x + x.e1.x; a[5] = x.m1.y + x.e1.y; a[6] = x.m1.z + x.e1.z; a[7] = x.m1.w + x.e1.w;
+  }
+}
+
+// Eight Q values Q[c..c+7][li] (zero past n or past the padded rank).
+struct Q8v { float4 a, b; };
+
+template <int RP>
+__device__ __forceinline__ Q8v q8_load(const float* qs, int n, int c, int li) {
+  float v[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) v[j] = (li < RP && c + j < n) ? qs[(int64_t)(c + j) * RP + li] : 0.f;
+  Q8v q;
+  q.a = make_float4(v[0], v[1], v[2], v[3]);
+  q.b = make_float4(v[4], v[5], v[6], v[7]);
+  return q;
+}
+
+// -------------------------------------------------------------------------
+// k_pm: left product on MFMA.  A block owns PM_ROWS whole rows; its eight
+// waves take interleaved 32-column K-steps of those rows (so together they
+// stream contiguous column ranges) and their partial tiles are summed in LDS
+// in wave order.  The block then stores its final rows of P and the fp64
+// Gram partial of those rows.
+// -------------------------------------------------------------------------
+struct PMSmem {
+  float red[PM_WAVES][PM_ROWS * 16];   // per-wave partial tiles
+  double rows[PM_ROWS * 16];           // final P rows as doubles (Gram)
+};
+
+template <int DT, bool VEC, int RP>
+__device__ __forceinline__ void pm_body(const Desc& d, int b, PMSmem& sm) {
+  const int wave = wave_id(), lane = threadIdx.x & 63;
+  const int li = lane & 15, g = lane >> 4;
+  const int row0 = b * PM_ROWS;
+  const int nk = (d.n + 31) / 32;
+  const float* qs = q_src<RP>(d);
+
+  // Blocks start their walk at staggered K-steps (and wrap around), so that
+  // at any moment the device reads many column ranges instead of one stripe
+  // of every row (which lands on a few HBM channels).
+  const int ks0 = (int)(((int64_t)b * PM_WAVES) % nk);
+  auto kcol = [&](int it) {
+    int k = ks0 + it;
+    if (k >= nk) k -= nk;
+    return 32 * k + 8 * g;
+  };
+
+  f4v acc[PM_RB];
+#pragma unroll
+  for (int r = 0; r < PM_RB; ++r) acc[r] = f4v{0.f, 0.f, 0.f, 0.f};
+
+  Ch8<DT> cur[PM_RB], nxt[PM_RB];
+  Q8v cq, nq;
+  int ks = wave;
+  if (ks < nk) {
+    const int c = kcol(ks);
+    cq = q8_load<RP>(qs, d.n, c, li);
+#pragma unroll
+    for (int r = 0; r < PM_RB; ++r) cur[r] = ch8_load<DT, VEC>(d, row0 + 16 * r + li, c, d.n);
+  }
+  for (; ks < nk; ks += PM_WAVES) {
+    const bool more = ks + PM_WAVES < nk;
+    const int cn = more ? kcol(ks + PM_WAVES) : 0;
+    if (more) {
+      nq = q8_load<RP>(qs, d.n, cn, li);
+#pragma unroll
+      for (int r = 0; r < PM_RB; ++r) nxt[r] = ch8_load<DT, VEC>(d, row0 + 16 * r + li, cn, d.n);
+    }
+    const float qv[8] = {cq.a.x, cq.a.y, cq.a.z, cq.a.w, cq.b.x, cq.b.y, cq.b.z, cq.b.w};
+#pragma unroll
+    for (int r = 0; r < PM_RB; ++r) {
+      float a[8];
+      ch8_values<DT>(cur[r], a);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[r] = mfma4(a[j], qv[j], acc[r]);
+    }
+    if (more) {
+      cq = nq;
+#pragma unroll
+      for (int r = 0; r < PM_RB; ++r) cur[r] = nxt[r];
+    }
+  }
+
+  // acc[r][v] = partial P[row0 + 16r + 4g + v][li] of this wave.
+#pragma unroll
+  for (int r = 0; r < PM_RB; ++r)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) sm.red[wave][(16 * r + 4 * g + v) * 16 + li] = acc[r][v];
+  __syncthreads();
+  const int nr = min(PM_ROWS, d.m - row0);
+  for (int e = threadIdx.x; e < PM_ROWS * RP; e += PM_THREADS) {
+    const int i = e / RP, k = e % RP;
+    float s = sm.red[0][i * 16 + k];
+#pragma unroll
+    for (int w = 1; w < PM_WAVES; ++w) s = s + sm.red[w][i * 16 + k];
+    if (i < nr) d.praw[(int64_t)(row0 + i) * RP + k] = s;
+    sm.rows[i * RP + k] = (i < nr) ? (double)s : 0.0;
+  }
+  __syncthreads();
+  gram_rows_store<RP, PM_THREADS>(sm.rows, nr, d.gpart + (int64_t)b * RP * RP);
+}
+
+template <int DT, bool VEC, int RP>
+__global__ __launch_bounds__(PM_THREADS) void k_pm(OCC_KARGS) {
+  __shared__ __attribute__((aligned(16))) PMSmem sm;
+#define B_(d, b) pm_body<DT, VEC, RP>(d, b, sm)
+  OCC_DISPATCH(K_PASS_P, B_)
+#undef B_
+}
+
+// -------------------------------------------------------------------------
+// k_qm: right product partials on MFMA.  A block owns 128 columns and a row
+// split; each wave takes a contiguous quarter of the split's rows in 4-row
+// K-steps.  The B operand is P_hat[row][li], read from the P_hat buffer.
+// The four waves' partial tiles are summed in LDS in wave order and stored
+// to qpart[split].
+// -------------------------------------------------------------------------
+struct QMSmem {
+  union {
+    float red[4 * QM_COLS * 16];    // per-wave partial tiles
+  } u;
+};
+
+template <int DT, bool VEC, int RP>
+__device__ __forceinline__ void qm_body(const Desc& d, int b, QMSmem& sm) {
+  const int wave = wave_id(), lane = threadIdx.x & 63;
+  const int li = lane & 15, g = lane >> 4;
+  const int col_tiles = (d.n + QM_COLS - 1) / QM_COLS;
+  const int ct = b % col_tiles, s = b / col_tiles;
+  const int r_lo = s * d.q_rows;
+  const int r_hi = min(d.m, r_lo + d.q_rows);
+  const int nr = r_hi - r_lo;
+  const int c0 = ct * QM_COLS;
+
+  const float* ps = p_src<RP>(d);
+
+  const int wr = (nr + 3) / 4;
+  const int w_lo = r_lo + min(nr, wave * wr), w_hi = r_lo + min(nr, wave * wr + wr);
+  const int nk = (w_hi - w_lo + 3) / 4;
+  const int col = c0 + 8 * li;
+  f4v acc[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) acc[t] = f4v{0.f, 0.f, 0.f, 0.f};
+  Ch8<DT> cur, nxt;
+  float cp = 0.f, np = 0.f;
+  {
+    const int row = w_lo + g;
+    const bool ok = row < w_hi;
+    cur = ch8_load<DT, VEC>(d, ok ? row : d.m, col, d.n);
+    cp = (ok && li < RP) ? ps[(int64_t)row * RP + li] : 0.f;
+  }
+  for (int ks = 0; ks < nk; ++ks) {
+    const bool more = ks + 1 < nk;
+    if (more) {
+      const int row = w_lo + 4 * (ks + 1) + g;
+      const bool ok = row < w_hi;
+      nxt = ch8_load<DT, VEC>(d, ok ? row : d.m, col, d.n);
+      np = (ok && li < RP) ? ps[(int64_t)row * RP + li] : 0.f;
+    }
+    float a[8];
+    ch8_values<DT>(cur, a);
+#pragma unroll
+    for (int t = 0; t < 8; ++t) acc[t] = mfma4(a[t], cp, acc[t]);
+    if (more) {
+      cur = nxt;
+      cp = np;
+    }
+  }
+
+  // acc[t][v] = partial Q[c0 + 8(4g + v) + t][li] of this wave.
+  float* red = sm.u.red + wave * (QM_COLS * 16);
+#pragma unroll
+  for (int t = 0; t < 8; ++t)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) red[(8 * (4 * g + v) + t) * 16 + li] = acc[t][v];
+  __syncthreads();
+  for (int e = threadIdx.x; e < QM_COLS * RP; e += kBlock) {
+    const int cl = e / RP, k = e % RP;
+    const int gcol = c0 + cl;
+    if (gcol >= d.n) continue;
+    float v = sm.u.red[cl * 16 + k];
+    v = v + sm.u.red[QM_COLS * 16 + cl * 16 + k];
+    v = v + sm.u.red[2 * QM_COLS * 16 + cl * 16 + k];
+    v = v + sm.u.red[3 * QM_COLS * 16 + cl * 16 + k];
+    d.qpart[((int64_t)s * d.n + gcol) * RP + k] = v;
+  }
+}
+
+template <int DT, bool VEC, int RP>
+__global__ __launch_bounds__(kBlock) void k_qm(OCC_KARGS) {
+  __shared__ __attribute__((aligned(16))) QMSmem sm;
+#define B_(d, b) qm_body<DT, VEC, RP>(d, b, sm)
+  OCC_DISPATCH(K_PASS_Q, B_)
+#undef B_
+}
+
+}  // namespace occ

@@ -56,6 +56,7 @@ struct Desc {
   float* ppart;          // sp x m x rp
   float* qpart;          // sq x n x rp
   double* gpart;         // ng x rp x rp
+  double* gsub;          // ceil(ng / 16) x rp x rp (group sums of the Gram tree)
   double* gsum;          // rp x rp
   double* t1;            // rp x rp
   double* tm;            // rp x rp
@@ -67,13 +68,15 @@ struct Desc {
   int32_t sp, p_cols;    // pass P: column splits and columns per split (multiple of PP_SUB)
   int32_t ng;            // Gram partial blocks (G_ROWS rows each)
   int32_t sq, q_rows;    // pass Q: row splits and rows per split
+  int32_t gb;            // fused path: blocks of the Gram-sum/Cholesky kernel
   int32_t blk[K_NUM];    // first block of this matrix in each kernel's grid
+  int32_t fused;         // 1: fused small-rank path (rank padded to <= 16)
   int32_t pad_;
 };
 
 // Tiling of one matrix (host side).
 struct Tiling {
-  int sp, p_cols, ng, sq, q_rows, n_pad;
+  int sp, p_cols, ng, sq, q_rows, n_pad, gb;
   int64_t blocks[K_NUM];
 };
 
@@ -86,20 +89,54 @@ inline int padded_rank(int r) {
   return p;
 }
 
-inline Tiling make_tiling(int64_t m, int64_t n, int rp) {
+// Fused small-rank path: tile constants shared with kernels_small.hpp.
+constexpr int kFusedMaxRank = 16;
+constexpr int F_PROWS = 32;       // left product: rows per block
+constexpr int F_QCOLS = 128;      // right product: columns per block
+constexpr int F_QMAXROWS = 512;   // right product: rows per block (P_hat rows in LDS)
+constexpr int F_MHROWS = 256;     // reconstruction: rows per block
+constexpr int F_MHCOLS = 256;     // reconstruction: columns per block (4 per lane)
+constexpr int F_QBLOCKS = 512;    // right product: target number of blocks
+constexpr int F_ORTHROWS = 128;   // Cholesky/P_hat kernel: rows of P_hat per block
+
+inline Tiling make_tiling(int64_t m, int64_t n, int rp, bool fused) {
   Tiling t{};
   t.n_pad = (int)round_up(n, PP_SUB);
-  // pass P: 64-row tiles; split the columns until there are ~1024 blocks,
-  // keeping at least 128 columns per split.
+  // pass P: 64-row tiles; split the columns until there are enough blocks,
+  // keeping at least 128 (fused: 256) columns per split.
   int64_t row_tiles = cdiv(m, PP_ROWS);
-  int64_t sp = cdiv(1024, row_tiles);
-  int64_t max_sp = cdiv(n, 128);
+  const int64_t p_blocks = fused ? cdiv(m, F_PROWS) : row_tiles;
+  int64_t sp = cdiv(1024, p_blocks);
+  int64_t max_sp = cdiv(n, fused ? 256 : 128);
   if (sp > max_sp) sp = max_sp;
   if (sp < 1) sp = 1;
   t.p_cols = (int)round_up(cdiv(n, sp), PP_SUB);
   t.sp = (int)cdiv(n, t.p_cols);
-  // Gram partials
-  t.ng = (int)cdiv(m, G_ROWS);
+  t.ng = fused ? (int)p_blocks : (int)cdiv(m, G_ROWS);
+  if (fused) {
+    // left product: whole rows per block, no column splits
+    t.sp = 1;
+    t.p_cols = (int)round_up(n, PP_SUB);
+    t.ng = (int)p_blocks;
+    t.gb = 1;
+    const int64_t col_tiles = cdiv(n, F_QCOLS);
+    int64_t sq = cdiv(F_QBLOCKS, col_tiles);
+    const int64_t max_sq = cdiv(m, 32);
+    if (sq > max_sq) sq = max_sq;
+    if (sq < 1) sq = 1;
+    t.q_rows = (int)round_up(cdiv(m, sq), 4);
+    t.sq = (int)cdiv(m, t.q_rows);
+    t.blocks[K_QPAD] = cdiv((int64_t)t.n_pad * rp, kBlock);
+    t.blocks[K_PASS_P] = p_blocks;
+    t.blocks[K_PGRAM] = cdiv(m, F_ORTHROWS);
+    t.blocks[K_GSUM] = 0;
+    t.blocks[K_GRAM2] = 0;
+    t.blocks[K_APPLY] = 0;
+    t.blocks[K_PASS_Q] = col_tiles * t.sq;
+    t.blocks[K_QRED] = cdiv(n * rp, kBlock);
+    t.blocks[K_MHAT] = cdiv(n, F_MHCOLS) * cdiv(m, F_MHROWS);
+    return t;
+  }
   // pass Q: column tiles of 64*cols_per_lane; row splits up to ~1024 blocks
   int cpl = cols_per_lane(rp);
   int64_t col_tiles = cdiv(n, (int64_t)kWave * cpl);
@@ -123,14 +160,15 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp) {
   return t;
 }
 
-// Workspace layout: [header 256 B][descriptor table][per-matrix regions].
+// Workspace layout: [header 256 B: sticky flags word][descriptor table]
+// [per-matrix regions].  occ_workspace_init zeroes the header.
 constexpr size_t kHeaderBytes = 256;
 constexpr size_t kAlign = 256;
 
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Regions {
-  size_t qpad, phat, praw, ppart, qpart, gpart, gsum, t1, tm, info, total;
+  size_t qpad, phat, praw, ppart, qpart, gpart, gsub, gsum, t1, tm, info, total;
 };
 
 inline Regions matrix_regions(int64_t m, int64_t n, int rp, const Tiling& t) {
@@ -143,6 +181,7 @@ inline Regions matrix_regions(int64_t m, int64_t n, int rp, const Tiling& t) {
   g.ppart = take((size_t)t.sp * m * rp * 4);
   g.qpart = take((size_t)t.sq * n * rp * 4);
   g.gpart = take((size_t)t.ng * rp * rp * 8);
+  g.gsub = take((size_t)(t.gb > 0 ? t.gb : cdiv(t.ng, 16)) * rp * rp * 8);
   g.gsum = take((size_t)rp * rp * 8);
   g.t1 = take((size_t)rp * rp * 8);
   g.tm = take((size_t)rp * rp * 8);

@@ -72,6 +72,19 @@ def test_config5_high_snr_small():
     assert_parity(res, "bf16", "act_grad high-SNR 700x520 r128 t2")
 
 
+@pytest.mark.parametrize("rank,iters,ratio", [(8, 2, 1.5), (16, 2, 1.2), (12, 3, 1.2), (32, 2, 1.1)])
+def test_ill_conditioned_iterates_second_pass(rank, iters, ratio):
+    """Geometric spectrum ratio^-j: the power iterates P have condition
+    number ratio^((2t-1)(r-1)) between 1e3 and 1e5, so the Cholesky diagonal
+    spans more than 1e3 and the CholeskyQR second pass runs.  (Much larger
+    condition numbers exceed what an fp32 P can resolve.)  The recipe's
+    "noise" field carries the ratio."""
+    w = Workload(93, "geom", ((400, 300),), "f32", rank, iters, 2, "geom",
+                 signal_rank=rank + 8, noise=ratio)
+    res, _, _ = run_workload(w, 2)
+    assert_parity(res, "f32", f"geometric {ratio}^-j r{rank} t{iters}")
+
+
 @pytest.mark.parametrize("shape,rank", [((1, 1), 1), ((5, 3), 3), ((64, 1), 1), ((1, 100), 1),
                                         ((65, 33), 8), ((3, 200), 2)])
 def test_tiny_shapes(shape, rank):

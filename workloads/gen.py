@@ -98,6 +98,16 @@ def lowrank_plus_noise(config: int, step: int, mat: int, m: int, n: int,
     return out
 
 
+def geometric_spectrum(config: int, step: int, mat: int, m: int, n: int, k: int,
+                       ratio: float) -> np.ndarray:
+    """U diag(ratio^-j, j=0..k-1) V^T (float64): a steeply decaying spectrum
+    whose power iterates are badly conditioned (exercises CholeskyQR2)."""
+    k = min(k, m, n)
+    u = haar(stream(config, step, mat, ROLE_U), m, k)
+    v = haar(stream(config, step, mat, ROLE_V), n, k)
+    return (u * ratio ** -np.arange(k, dtype=np.float64)) @ v.T
+
+
 def zipf_rows(config: int, step: int, mat: int, vocab: int, hidden: int,
               tokens: int, exponent: float = 1.1, std: float = 1e-2) -> np.ndarray:
     """Embedding-gradient rows: `tokens` Zipf ids, each adding an N(0, std) row.
@@ -131,7 +141,7 @@ class Workload:
     rank: int
     iters: int
     steps: int
-    kind: str              # recipe: gauss | lowrank | zipf | gauss1024
+    kind: str              # recipe: gauss | lowrank | zipf | geom | gauss1024
     std: float = 1.0
     signal_rank: int = 0
     noise: float = 0.0
@@ -160,6 +170,8 @@ class Workload:
                                    self.signal_scale)
         elif self.kind == "zipf":
             x = zipf_rows(c, step, j, m, n, self.tokens)
+        elif self.kind == "geom":
+            x = geometric_spectrum(c, step, j, m, n, self.signal_rank, self.noise)
         else:
             raise ValueError(self.kind)
         return to_stored(x, self.m_dtype)
