@@ -35,14 +35,15 @@ sys.path.insert(0, ROOT)
 METRIC = "compress+decompress+err-update input GB/s and % of HBM roofline, 1 MI355X"
 HBM_PEAK_GBS = 8000.0
 PROFILES = os.path.join(ROOT, "profiles")
-KERNEL_SOURCES = ["paper_2301_09830_amd/csrc/kernels.hpp", "paper_2301_09830_amd/csrc/plan.hpp",
-                  "paper_2301_09830_amd/csrc/api.hip"]
+CSRC = os.path.join(ROOT, "paper_2301_09830_amd", "csrc")
 
 
 def kernel_source_digest() -> str:
+    """Digest of the library sources; counter summaries apply only to it."""
     h = hashlib.sha256()
-    for rel in KERNEL_SOURCES:
-        with open(os.path.join(ROOT, rel), "rb") as f:
+    for path in sorted(glob.glob(os.path.join(CSRC, "*.hpp")) + glob.glob(os.path.join(CSRC, "*.hip"))):
+        with open(path, "rb") as f:
+            h.update(os.path.basename(path).encode())
             h.update(f.read())
     return h.hexdigest()[:16]
 
@@ -140,6 +141,85 @@ def cpu_baseline(w, host, seconds: float):
                       f"carried err/Q) on {cores} BLAS threads"}
 
 
+# ----------------------------------------------------------------------------
+# rocprofv3 summaries -> profiles/ (host-side text processing, no GPU)
+# ----------------------------------------------------------------------------
+PROFILE_KERNELS = {  # library kernel -> name used in per-kernel timings
+    "k_mh16": "mhat_err", "k_pm": "pass_p", "k_qm": "pass_q", "k_orth16": "orth",
+    "k_qred16": "q_reduce",
+}
+
+
+def _short(kname: str) -> str:
+    base = kname.split("(")[0].replace("void ", "").replace("occ::", "")
+    return base.split("<")[0]
+
+
+def write_profiles(workload: str, trace_dir: str, fetch_dir: str, write_dir: str,
+                   commands: dict, elements: int, m_bytes: int) -> list:
+    """Summaries of one rocprofv3 kernel trace and two counter runs."""
+    import csv
+    out = []
+    stats = glob.glob(os.path.join(trace_dir, "*kernel_stats.csv"))[0]
+    rows = list(csv.DictReader(open(stats)))
+    lines = ["| kernel | calls | avg us | min us | max us | share % |", "|---|---|---|---|---|---|"]
+    for r in rows:
+        lines.append(f"| `{r['Name'].split('(')[0]}` | {r['Calls']} | {float(r['AverageNs'])/1e3:.2f} | "
+                     f"{float(r['MinNs'])/1e3:.2f} | {float(r['MaxNs'])/1e3:.2f} | {float(r['Percentage']):.1f} |")
+
+    def counters(d):
+        agg = {}
+        for r in csv.DictReader(open(glob.glob(os.path.join(d, "*counter_collection.csv"))[0])):
+            agg.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return {k: sum(v) / len(v) for k, v in agg.items()}
+    fetch, write = counters(fetch_dir), counters(write_dir)
+    copy = [k for k in fetch if "copyBuffer" in k or "copy" in k.lower()]
+    cal_read = cal_write = None
+    calib_bytes = commands.get("calibration_bytes")
+    if copy and calib_bytes:
+        k = copy[0]
+        cal_read = calib_bytes / (fetch[k] * 1024.0)
+        cal_write = calib_bytes / (write[k] * 1024.0)
+    digest = kernel_source_digest()
+    for r in rows:
+        short = _short(r["Name"])
+        name = PROFILE_KERNELS.get(short)
+        if name is None:
+            continue
+        fk = next((k for k in fetch if k.split("(")[0] == r["Name"].split("(")[0]), None)
+        rec = {"kernel": name, "hip_kernel": r["Name"].split("(")[0], "workload": workload,
+               "avg_duration_us": round(float(r["AverageNs"]) / 1e3, 3),
+               "kernel_source_sha": digest}
+        if fk is not None and cal_read:
+            rb = fetch[fk] * 1024.0 * cal_read
+            wb = write[fk] * 1024.0 * cal_write
+            rec.update(fetch_kib_per_dispatch=round(fetch[fk], 3), write_kib_per_dispatch=round(write[fk], 3),
+                       read_calibration=round(cal_read, 4), write_calibration=round(cal_write, 4),
+                       hbm_bytes_per_launch=int(rb + wb))
+            alg = kernel_alg_bytes(name, elements, m_bytes)
+            if alg:
+                rec["alg_bytes_per_launch"] = alg
+        text = [f"# `{name}` on {workload}: rocprofv3 summary", "",
+                f"Kernel `{rec['hip_kernel']}`; average duration {rec['avg_duration_us']} us "
+                f"over {r['Calls']} dispatches.", "",
+                "Commands (run from the repository root on the MI355X box):", ""]
+        for key in ("trace", "fetch", "write"):
+            text.append(f"- {key}: `{commands[key]}`")
+        text += ["", "Kernel trace statistics of the same run (all kernels of the step):", ""] + lines
+        if "hbm_bytes_per_launch" in rec:
+            text += ["", f"HBM traffic per dispatch: FETCH_SIZE {rec['fetch_kib_per_dispatch']} KiB x "
+                         f"{rec['read_calibration']} + WRITE_SIZE {rec['write_kib_per_dispatch']} KiB x "
+                         f"{rec['write_calibration']} = {rec['hbm_bytes_per_launch']} bytes. The calibration "
+                         "factors are (bytes a plain device copy of known size moves) / (what the counter "
+                         "reports for that copy)."]
+        text += ["", "```json", json.dumps(rec, indent=1), "```", ""]
+        path = os.path.join(PROFILES, f"{name}__{workload}__pmc.md")
+        with open(path, "w") as f:
+            f.write("\n".join(text))
+        out.append(path)
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -153,7 +233,19 @@ def main() -> int:
     ap.add_argument("--no-kernel-timing", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this size (counter calibration)")
+    ap.add_argument("--write-profiles", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
+                    help="host only: turn rocprofv3 csv output into profiles/*.md summaries")
+    ap.add_argument("--profile-commands", default="",
+                    help="json {trace, fetch, write, calibration_bytes} recorded in the summaries")
     args = ap.parse_args()
+
+    if args.write_profiles:
+        from workloads import WORKLOADS
+        w = WORKLOADS[args.workload]
+        paths = write_profiles(w.name, *args.write_profiles, json.loads(args.profile_commands),
+                               w.elements, 2 if w.m_dtype == "bf16" else 4)
+        print("\n".join(paths))
+        return 0
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(json.dumps({"metric": METRIC, "error": "liboptcc runs on one GPU; "
