@@ -16,6 +16,7 @@
 #include "kernels.hpp"
 #include "kernels_small.hpp"
 #include "kernels_mfma16.hpp"
+#include "kernels_large.hpp"
 
 using namespace occ;
 
@@ -163,11 +164,11 @@ void finalize_regions(Batch& b, void* ws) {
     d.ppart = (float*)(base + (uintptr_t)d.ppart);
     d.qpart = (float*)(base + (uintptr_t)d.qpart);
     d.gpart = (double*)(base + (uintptr_t)d.gpart);
-    d.gsub = (double*)(base + (uintptr_t)d.gsub);
     d.gsum = (double*)(base + (uintptr_t)d.gsum);
     d.t1 = (double*)(base + (uintptr_t)d.t1);
     d.tm = (double*)(base + (uintptr_t)d.tm);
     d.info = (uint32_t*)(base + (uintptr_t)d.info);
+    d.phat_t = (float*)(base + (uintptr_t)d.phat_t);
   }
 }
 
@@ -200,7 +201,7 @@ occ_status_t plan_batch(const occ_mat_t* mats, int count, int rank, int iters, u
   for (int k = 0; k < K_NUM; ++k) b.blocks[k] = 0;
   for (int j = 0; j < count; ++j) {
     const occ_mat_t& a = mats[j];
-    const Tiling t = make_tiling(a.rows, a.cols, b.rp, b.fused);
+    const Tiling t = make_tiling(a.rows, a.cols, b.rp);
     const Regions g = matrix_regions(a.rows, a.cols, b.rp, t);
     Desc& d = b.descs[j];
     d.m = (int32_t)a.rows;
@@ -212,7 +213,8 @@ occ_status_t plan_batch(const occ_mat_t* mats, int count, int rank, int iters, u
     d.ng = t.ng;
     d.sq = t.sq;
     d.q_rows = t.q_rows;
-    d.gb = t.gb;
+    d.m_pad = t.m_pad;
+    d.mr = t.mr;
     d.fused = b.fused ? 1 : 0;
     for (int k = 0; k < K_NUM; ++k) {
       d.blk[k] = (int32_t)b.blocks[k];
@@ -226,11 +228,11 @@ occ_status_t plan_batch(const occ_mat_t* mats, int count, int rank, int iters, u
     d.ppart = (float*)(uintptr_t)(off + g.ppart);
     d.qpart = (float*)(uintptr_t)(off + g.qpart);
     d.gpart = (double*)(uintptr_t)(off + g.gpart);
-    d.gsub = (double*)(uintptr_t)(off + g.gsub);
     d.gsum = (double*)(uintptr_t)(off + g.gsum);
     d.t1 = (double*)(uintptr_t)(off + g.t1);
     d.tm = (double*)(uintptr_t)(off + g.tm);
     d.info = (uint32_t*)(uintptr_t)(off + g.info);
+    d.phat_t = (float*)(uintptr_t)(off + g.phat_t);
     off += g.total;
   }
   b.ws_needed = off;
@@ -276,6 +278,7 @@ occ_status_t plan_batch(const occ_mat_t* mats, int count, int rank, int iters, u
     d.lde_in = (int32_t)a.lde;
     d.lde_out = (int32_t)a.lde;
     d.ldh = write_mhat ? (int32_t)a.ldh : 0;
+    d.vec = vec ? 1 : 0;
   }
   return OCC_OK;
 }
@@ -336,24 +339,39 @@ occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, h
           return;
         }
       }
-      L("qpad", k_qpad<RP>, b.blocks[K_QPAD]);
-      for (int it = 0; it < b.iters; ++it) {
-        L("pass_p", k_pass_p<DT, VEC, RP>, b.blocks[K_PASS_P]);
-        L("gram", k_gram<RP, 0>, b.blocks[K_PGRAM]);
-        L("gram_sum", k_gsum<RP, 0>, b.blocks[K_GSUM]);
-        L("chol", k_chol<RP, 0>, count, flags);
-        L("gram2", k_gram<RP, 1>, b.blocks[K_GRAM2]);
-        L("gram_sum2", k_gsum<RP, 1>, b.blocks[K_GSUM]);
-        L("chol2", k_chol<RP, 1>, count, flags);
-        L("apply", k_apply<RP>, b.blocks[K_APPLY]);
-        L("pass_q", k_pass_q<DT, VEC, RP>, b.blocks[K_PASS_Q]);
-        L("q_reduce", k_qred<RP>, b.blocks[K_QRED]);
-      }
-      if (finish) {
-        if (write_mhat)
-          L("mhat_err", k_mhat<DT, VEC, RP, 0, true, true>, b.blocks[K_MHAT]);
-        else
-          L("err_only", k_mhat<DT, VEC, RP, 0, false, true>, b.blocks[K_MHAT]);
+      if constexpr (RP > kFusedMaxRank) {
+        // Large-rank path.  With an error buffer to write (fused step) the
+        // first left product stores A over it and every later pass reads A
+        // back from there; a compress-only call re-reads M and err_prev.
+        const bool saved = b.descs[0].err_out != nullptr;
+        L("qpad", k_qpad<RP>, b.blocks[K_QPAD]);
+        for (int it = 0; it < b.iters; ++it) {
+          if (!saved)
+            L("pass_p", k_lp<DT, RP, SA_MERR>, b.blocks[K_PASS_P]);
+          else if (it == 0)
+            L("pass_p_first", k_lp<DT, RP, SA_MERR_SAVE>, b.blocks[K_PASS_P]);
+          else
+            L("pass_p", k_lp<DT_F32, RP, SA_SAVED>, b.blocks[K_PASS_P]);
+          L("gram", k_lg<RP, 0>, b.blocks[K_PGRAM]);
+          L("gram_sum", k_gsum<RP, 0>, b.blocks[K_GSUM]);
+          LB("chol", k_lchol<RP, 0>, count, LC_THREADS, flags);
+          L("apply", k_lapply<RP, 0>, b.blocks[K_APPLY]);
+          L("gram2", k_lg<RP, 1>, b.blocks[K_GRAM2]);
+          L("gram_sum2", k_gsum<RP, 1>, b.blocks[K_GSUM]);
+          LB("chol2", k_lchol<RP, 1>, count, LC_THREADS, flags);
+          L("apply2", k_lapply<RP, 1>, b.blocks[K_APPLY]);
+          if (saved)
+            L("pass_q", k_lq<DT_F32, RP, SA_SAVED>, b.blocks[K_PASS_Q]);
+          else
+            L("pass_q", k_lq<DT, RP, SA_MERR>, b.blocks[K_PASS_Q]);
+          L("q_reduce", k_qred<RP>, b.blocks[K_QRED]);
+        }
+        if (finish) {
+          if (write_mhat)
+            L("mhat_err", k_ml<DT_F32, RP, SA_SAVED, 0, true, true>, b.blocks[K_MHAT]);
+          else
+            L("err_only", k_ml<DT_F32, RP, SA_SAVED, 0, false, true>, b.blocks[K_MHAT]);
+        }
       }
     });
   });
@@ -465,6 +483,7 @@ occ_status_t occ_compress(const void* M, int m_dtype, int64_t m, int64_t n, int6
   d.Mhat = nullptr;
   b.vec = aligned(M, 16) && ldm % (m_dtype == OCC_BF16 ? 8 : 4) == 0 &&
           (!err_prev || (aligned(err_prev, 16) && lde % 4 == 0));
+  d.vec = b.vec ? 1 : 0;
   return run_batch(b, ws, false, false, (hipStream_t)stream);
 }
 
@@ -478,7 +497,7 @@ occ_status_t occ_decompress(const float* P, const float* Q, int64_t m, int64_t n
                              span2d(M_hat, m, n, ldh, 4, true)};
   if (overlaps(spans)) return OCC_E_ALIAS;
   const int rp = padded_rank(rank);
-  const Tiling t = make_tiling(m, n, rp, false);
+  const Tiling t = make_tiling(m, n, rp);
   Desc d{};
   d.m = (int32_t)m;
   d.n = (int32_t)n;
@@ -487,20 +506,27 @@ occ_status_t occ_decompress(const float* P, const float* Q, int64_t m, int64_t n
   d.Q = const_cast<float*>(Q);
   d.Mhat = M_hat;
   d.ldh = (int32_t)ldh;
+  d.mr = t.mr;
   const bool vec = aligned(M_hat, 16) && ldh % 4 == 0;
   hipStream_t s = (hipStream_t)stream;
   occ_status_t st = OCC_OK;
   with_rp(rp, [&](auto RPc) {
     constexpr int RP = decltype(RPc)::value;
     st = launch("decompress", s, [&] {
-      if (vec)
+      if constexpr (RP > kFusedMaxRank) {
+        // same products as the fused step's reconstruction pass
+        hipLaunchKernelGGL((k_ml<DT_F32, RP, SA_SAVED, 1, true, false>),
+                           dim3(grid_of(t.blocks[K_MHAT])), dim3(kBlock), 0, s,
+                           (const Desc*)nullptr, 1, d);
+      } else if (vec) {
         hipLaunchKernelGGL((k_mhat<DT_F32, true, RP, 1, true, false>),
-                           dim3(grid_of(t.blocks[K_MHAT])), dim3(kBlock), 0, s,
+                           dim3(grid_of(mhat_blocks(m, n, RP))), dim3(kBlock), 0, s,
                            (const Desc*)nullptr, 1, d);
-      else
+      } else {
         hipLaunchKernelGGL((k_mhat<DT_F32, false, RP, 1, true, false>),
-                           dim3(grid_of(t.blocks[K_MHAT])), dim3(kBlock), 0, s,
+                           dim3(grid_of(mhat_blocks(m, n, RP))), dim3(kBlock), 0, s,
                            (const Desc*)nullptr, 1, d);
+      }
     });
   });
   return st;

@@ -1,0 +1,844 @@
+// Large-rank path (padded rank RP = 32, 64 or 128) on the matrix cores.
+//
+// Every product of a power-iteration round is a dense contraction with a
+// 32..128-wide factor, so all three streaming passes run on
+// v_mfma_f32_32x32x2_f32 (fp32 operands, fp32 accumulation).  Lane layout
+// (lane l = 32*g + li):
+//   A operand  a = A[i = li][k = g]       B operand  b = B[k = g][j = li]
+//   result     D[i = 8*(v/4) + 4*g + v%4][j = li] in component v (16 floats)
+// so each half-wave of an output register holds 32 consecutive columns of
+// one row.
+//
+// A pass takes A = M + err_prev from one of three places (template SA):
+//   SA_MERR       M and err_prev, added on the fly (compress-only calls);
+//   SA_MERR_SAVE  the same, and the pass stores A over err (first left
+//                 product of a fused step: the error buffer is about to be
+//                 replaced by A - M_hat anyway);
+//   SA_SAVED      A read back from the error buffer (every later pass of a
+//                 fused step), 4 bytes per element instead of s_M + 4.
+// The stored A is exactly the fp32 sum the other modes form in registers, so
+// all three give bitwise the same products.
+//
+//   k_lp      P partials = A Q.  A block owns 128 rows (32 per wave) and a
+//             column split; its waves walk the same 32-column K-steps, the
+//             Q tile of the step staged once in LDS.  Lane (g, li) loads 16
+//             consecutive columns of its row and feeds 16 MFMAs per rank
+//             tile.  Output ranks are interleaved (lane li of rank tile u
+//             holds rank RP/32*li + u) so one LDS vector read gives a lane
+//             all its B values and one vector store writes its P values.
+//   k_lg      P = sum of the splits (stored), fp64 Gram partial of 256 rows.
+//   k_lchol   one block per matrix: T = R^-1 of the Gram G = R^T R (fp64),
+//             right-looking, one barrier per column.
+//   k_lapply  P_hat = P T (fp64 arithmetic, fp32 result), also stored
+//             transposed for the reconstruction pass.
+//   k_lq      Q partials = A^T P_hat over row splits; the waves of a block
+//             own adjacent column strips and share the P_hat rows of each
+//             8-row step through LDS.
+//   k_ml      M_hat = P_hat Q^T and err = A - M_hat; a wave keeps its Q
+//             columns in registers and walks 32-row tiles whose P_hat block
+//             is staged (transposed) in LDS.
+#pragma once
+
+#include "kernels_mfma16.hpp"
+
+namespace occ {
+
+typedef float f16v __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ f16v mfma32(float a, float b, f16v c) {
+  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
+
+// Row inside a 32x32 MFMA tile of accumulator component v, lanes of half g.
+__device__ __forceinline__ constexpr int mf32_row(int v, int g) {
+  return 8 * (v >> 2) + 4 * g + (v & 3);
+}
+
+enum { SA_MERR = 0, SA_MERR_SAVE = 1, SA_SAVED = 2 };
+
+// W consecutive floats / 32-bit words (W a power of two, naturally aligned).
+template <int W>
+__device__ __forceinline__ void ld_f(const float* p, float* o) {
+  if constexpr (W == 1) {
+    o[0] = *p;
+  } else if constexpr (W == 2) {
+    const float2 v = *(const float2*)p;
+    o[0] = v.x; o[1] = v.y;
+  } else {
+#pragma unroll
+    for (int j = 0; j < W; j += 4) {
+      const float4 v = *(const float4*)(p + j);
+      o[j] = v.x; o[j + 1] = v.y; o[j + 2] = v.z; o[j + 3] = v.w;
+    }
+  }
+}
+
+template <int W>
+__device__ __forceinline__ void ld_u(const uint32_t* p, uint32_t* o) {
+  if constexpr (W == 1) {
+    o[0] = *p;
+  } else if constexpr (W == 2) {
+    const uint2 v = *(const uint2*)p;
+    o[0] = v.x; o[1] = v.y;
+  } else {
+#pragma unroll
+    for (int j = 0; j < W; j += 4) {
+      const uint4 v = *(const uint4*)(p + j);
+      o[j] = v.x; o[j + 1] = v.y; o[j + 2] = v.z; o[j + 3] = v.w;
+    }
+  }
+}
+
+template <int W>
+__device__ __forceinline__ void st_f(float* p, const float* v) {
+  if constexpr (W == 1) {
+    *p = v[0];
+  } else if constexpr (W == 2) {
+    *(float2*)p = make_float2(v[0], v[1]);
+  } else {
+#pragma unroll
+    for (int j = 0; j < W; j += 4) *(float4*)(p + j) = make_float4(v[j], v[j + 1], v[j + 2], v[j + 3]);
+  }
+}
+
+// W consecutive elements of A (columns c..c+W-1 of one row) as raw loads,
+// converted only when used so that the loads stay in flight.  Elements that
+// are out of range, or that the vector path cannot take, hold the exact A
+// value (0 out of range) in e and -0 in m (x + -0 == x for every x).
+template <int DT, int SA, int W>
+struct RawA {
+  static constexpr int MW = SA == SA_SAVED ? 1 : (DT == DT_BF16 ? (W >= 2 ? W / 2 : 1) : W);
+  uint32_t m[MW];
+  float e[W];
+};
+
+template <int DT, int SA, int W>
+__device__ __forceinline__ RawA<DT, SA, W> rawa_load(const Desc& d, bool vec, int row, int c,
+                                                    int c_hi) {
+  RawA<DT, SA, W> x;
+  if (vec && row < d.m && c + W <= c_hi) {
+    if constexpr (SA == SA_SAVED) {
+      ld_f<W>(d.err_out + (int64_t)row * d.lde_out + c, x.e);
+      x.m[0] = 0u;
+    } else {
+      if constexpr (DT == DT_BF16) {
+        const uint16_t* mp = (const uint16_t*)d.M + (int64_t)row * d.ldm + c;
+        if constexpr (W == 1) x.m[0] = (uint32_t)(*mp) << 16;
+        else ld_u<W / 2>((const uint32_t*)mp, x.m);
+      } else {
+        ld_u<W>((const uint32_t*)((const float*)d.M + (int64_t)row * d.ldm + c), x.m);
+      }
+      if (d.err_in) {
+        ld_f<W>(d.err_in + (int64_t)row * d.lde_in + c, x.e);
+      } else {
+#pragma unroll
+        for (int j = 0; j < W; ++j) x.e[j] = -0.f;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < W; ++j) {
+      float v = 0.f;
+      if (row < d.m && c + j < c_hi) {
+        if constexpr (SA == SA_SAVED) {
+          v = d.err_out[(int64_t)row * d.lde_out + c + j];
+        } else {
+          v = m_elem<DT>(d, (int64_t)row * d.ldm + c + j);
+          if (d.err_in) v = v + d.err_in[(int64_t)row * d.lde_in + c + j];
+        }
+      }
+      x.e[j] = v;
+    }
+    const uint32_t nz = (SA != SA_SAVED && DT == DT_BF16 && W >= 2) ? 0x80008000u : 0x80000000u;
+#pragma unroll
+    for (int w = 0; w < RawA<DT, SA, W>::MW; ++w) x.m[w] = nz;
+  }
+  return x;
+}
+
+template <int DT, int SA, int W>
+__device__ __forceinline__ float rawa_val(const RawA<DT, SA, W>& x, int j) {
+  if constexpr (SA == SA_SAVED) {
+    return x.e[j];
+  } else if constexpr (DT == DT_BF16) {
+    if constexpr (W == 1) return __uint_as_float(x.m[0]) + x.e[0];
+    else return ((j & 1) ? bf16_hi(x.m[j >> 1]) : bf16_lo(x.m[j >> 1])) + x.e[j];
+  } else {
+    return __uint_as_float(x.m[j]) + x.e[j];
+  }
+}
+
+// Store W values of A over the error buffer (row < m).
+template <int W>
+__device__ __forceinline__ void a_store(const Desc& d, bool vec, int row, int c, int c_hi,
+                                        const float* a) {
+  if (row >= d.m) return;
+  float* p = d.err_out + (int64_t)row * d.lde_out + c;
+  if (vec && c + W <= c_hi) {
+    st_f<W>(p, a);
+  } else {
+#pragma unroll
+    for (int j = 0; j < W; ++j)
+      if (c + j < c_hi) p[j] = a[j];
+  }
+}
+
+// -------------------------------------------------------------------------
+// k_lp: P partials = A Q for one 128-row tile and one column split.
+// -------------------------------------------------------------------------
+template <int RP>
+struct LPSmem {
+  float q[2][L_KC * (RP + 4)];   // Q rows of the current and next K-step
+};
+
+template <int DT, int RP, int SA>
+__device__ __forceinline__ void lp_body(const Desc& d, int b, LPSmem<RP>& sm) {
+  constexpr int NU = RP / 32;               // rank tiles
+  constexpr int QP = RP + 4;                // LDS pitch of a Q row
+  constexpr int QF4 = L_KC * RP / 4 / kBlock;  // float4s per thread per Q tile
+  static_assert(QF4 * 4 * kBlock == L_KC * RP, "Q tile must split evenly");
+  const bool vec = d.vec != 0;
+  const int wave = wave_id(), lane = threadIdx.x & 63;
+  const int li = lane & 31, g = lane >> 5;
+  const int row_tiles = (d.m + L_PROWS - 1) / L_PROWS;
+  const int rt = b % row_tiles, s = b / row_tiles;
+  const int row = rt * L_PROWS + 32 * wave + li;
+  const int c_lo = s * d.p_cols;
+  const int c_hi = min(d.n, c_lo + d.p_cols);
+  const int nk = (c_hi - c_lo + L_KC - 1) / L_KC;
+  // Row tiles start their walk at staggered K-steps (and wrap around) so the
+  // device does not read one column stripe of every row at a time.
+  const int ks0 = (int)(((int64_t)rt * 4) % nk);
+
+  f16v acc[NU];
+#pragma unroll
+  for (int u = 0; u < NU; ++u) acc[u] = f16v{};
+
+  // qpad has n_pad (a multiple of 32) rows, so every K-step's Q tile is in
+  // bounds; its rows past n are zero.
+  f4v qr[QF4];
+  int kc = c_lo + L_KC * ks0;
+#pragma unroll
+  for (int x = 0; x < QF4; ++x)
+    qr[x] = *(const f4v*)(d.qpad + (int64_t)kc * RP + 4 * (threadIdx.x + kBlock * x));
+#pragma unroll
+  for (int x = 0; x < QF4; ++x) {
+    const int f = 4 * (threadIdx.x + kBlock * x);
+    *(f4v*)(&sm.q[0][(f / RP) * QP + f % RP]) = qr[x];
+  }
+  RawA<DT, SA, 16> cur = rawa_load<DT, SA, 16>(d, vec, row, kc + 16 * g, c_hi), nxt;
+  __syncthreads();
+
+  for (int it = 0; it < nk; ++it) {
+    const bool more = it + 1 < nk;
+    int kn = 0;
+    if (more) {
+      int k = ks0 + it + 1;
+      if (k >= nk) k -= nk;
+      kn = c_lo + L_KC * k;
+#pragma unroll
+      for (int x = 0; x < QF4; ++x)
+        qr[x] = *(const f4v*)(d.qpad + (int64_t)kn * RP + 4 * (threadIdx.x + kBlock * x));
+      nxt = rawa_load<DT, SA, 16>(d, vec, row, kn + 16 * g, c_hi);
+    }
+    float a[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) a[j] = rawa_val<DT, SA, 16>(cur, j);
+    if constexpr (SA == SA_MERR_SAVE) a_store<16>(d, vec, row, kc + 16 * g, c_hi, a);
+    const float* qb = sm.q[it & 1] + 16 * g * QP + NU * li;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      float bv[NU];
+      ld_f<NU>(qb + j * QP, bv);
+#pragma unroll
+      for (int u = 0; u < NU; ++u) acc[u] = mfma32(a[j], bv[u], acc[u]);
+    }
+    if (more) {
+#pragma unroll
+      for (int x = 0; x < QF4; ++x) {
+        const int f = 4 * (threadIdx.x + kBlock * x);
+        *(f4v*)(&sm.q[(it + 1) & 1][(f / RP) * QP + f % RP]) = qr[x];
+      }
+      cur = nxt;
+      kc = kn;
+    }
+    __syncthreads();
+  }
+
+  // acc[u][v] = P[rt*128 + 32*wave + mf32_row(v, g)][NU*li + u] (this split)
+  float* dst = d.ppart + (int64_t)s * d.m * RP;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int r = rt * L_PROWS + 32 * wave + mf32_row(v, g);
+    if (r < d.m) {
+      float o[NU];
+#pragma unroll
+      for (int u = 0; u < NU; ++u) o[u] = acc[u][v];
+      st_f<NU>(dst + (int64_t)r * RP + NU * li, o);
+    }
+  }
+}
+
+template <int DT, int RP, int SA>
+__global__ __launch_bounds__(kBlock) void k_lp(OCC_KARGS) {
+  __shared__ __attribute__((aligned(16))) LPSmem<RP> sm;
+#define B_(d, b) lp_body<DT, RP, SA>(d, b, sm)
+  OCC_DISPATCH(K_PASS_P, B_)
+#undef B_
+}
+
+// -------------------------------------------------------------------------
+// k_lg: Gram partial of 256 rows in fp64.  MODE 0: the rows are P (sum of
+// the left product's column splits, stored to praw).  MODE 1 (second
+// CholeskyQR pass, skipped unless the first pass asked for it): the rows
+// are the first pass's P_hat.  Each thread owns an (RP/16)^2 tile of G.
+// -------------------------------------------------------------------------
+template <int RP>
+struct LGSmem {
+  double rows[32][RP + 2];
+};
+
+template <int RP, int MODE>
+__device__ __forceinline__ void lg_body(const Desc& d, int b, LGSmem<RP>& sm) {
+  if (MODE == 1 && !d.info[0]) return;
+  constexpr int TS = RP / 16;
+  const int t = threadIdx.x, ta = t >> 4, tb = t & 15;
+  double acc[TS][TS];
+#pragma unroll
+  for (int p = 0; p < TS; ++p)
+#pragma unroll
+    for (int q = 0; q < TS; ++q) acc[p][q] = 0.0;
+  const int r_lo = b * L_GROWS, r_hi = min(d.m, r_lo + L_GROWS);
+  for (int c0 = r_lo; c0 < r_hi; c0 += 32) {
+    const int nr = min(32, r_hi - c0);
+    for (int idx = t; idx < 32 * RP; idx += kBlock) {
+      const int i = idx / RP, k = idx % RP;
+      double v = 0.0;
+      if (i < nr) {
+        const int64_t row = c0 + i;
+        if (MODE == 0) {
+          float s = d.ppart[row * RP + k];
+          for (int p = 1; p < d.sp; ++p) s = s + d.ppart[((int64_t)p * d.m + row) * RP + k];
+          d.praw[row * RP + k] = s;
+          v = (double)s;
+        } else {
+          v = (double)d.phat[row * RP + k];
+        }
+      }
+      sm.rows[i][k] = v;
+    }
+    __syncthreads();
+    for (int i = 0; i < nr; ++i) {
+      double x[TS], y[TS];
+#pragma unroll
+      for (int q = 0; q < TS; ++q) {
+        x[q] = sm.rows[i][TS * ta + q];
+        y[q] = sm.rows[i][TS * tb + q];
+      }
+#pragma unroll
+      for (int p = 0; p < TS; ++p)
+#pragma unroll
+        for (int q = 0; q < TS; ++q) acc[p][q] = fma(x[p], y[q], acc[p][q]);
+    }
+    __syncthreads();
+  }
+  double* gp = d.gpart + (int64_t)b * RP * RP;
+#pragma unroll
+  for (int p = 0; p < TS; ++p)
+#pragma unroll
+    for (int q = 0; q < TS; ++q) gp[(TS * ta + p) * RP + TS * tb + q] = acc[p][q];
+}
+
+template <int RP, int MODE>
+__global__ __launch_bounds__(kBlock) void k_lg(OCC_KARGS) {
+  __shared__ __attribute__((aligned(16))) LGSmem<RP> sm;
+#define B_(d, b) lg_body<RP, MODE>(d, b, sm)
+  OCC_DISPATCH(MODE == 0 ? K_PGRAM : K_GRAM2, B_)
+#undef B_
+}
+
+// -------------------------------------------------------------------------
+// k_lchol: T = R^-1 with G = R^T R (fp64), one block of 1024 threads per
+// matrix.  Thread (bi, bk) keeps the (RP/32)^2 blocks of the working Gram W
+// (upper triangle) and of T at rows RP/32*bi.., columns RP/32*bk.. in
+// registers.  Step j: the owners publish row j of W and column j of T
+// through LDS, then every thread applies
+//   W[i][k] -= W[j][i] W[j][k] / W[j][j]      (j < i <= k)
+//   T[l][k] -= T[l][j] W[j][k] / W[j][j]      (l <= j < k)
+// which is the right-looking Cholesky of G together with the column
+// recurrence of its inverse factor; finally T[:, k] /= sqrt(pivot k).
+// A pivot <= kPivotTol * max diag(G), or a padding column (k >= r), is
+// dependent: its column of T is zero and it updates nothing.
+//   MODE 0: T -> t1; decide whether a second pass is needed (info[0]).
+//   MODE 1: only when info[0]; T of the first pass's P_hat -> tm.
+// -------------------------------------------------------------------------
+constexpr int LC_THREADS = 1024;
+
+template <int RP>
+struct LCSmem {
+  double roww[2][RP];
+  double colt[2][RP];
+  double diag[RP];     // diag(G), then sqrt of each pivot (0 when dependent)
+  int dep[RP];
+  double thr;
+};
+
+template <int RP, int MODE>
+__device__ __forceinline__ void lchol_body(const Desc& d, uint32_t* flags, LCSmem<RP>& sm) {
+  if (MODE == 1 && !d.info[0]) return;
+  constexpr int BS = RP / 32;
+  const int t = threadIdx.x, bi = t >> 5, bk = t & 31;
+  const int i0 = BS * bi, k0 = BS * bk;
+  const int r = d.r;
+  double W[BS][BS], T[BS][BS];
+#pragma unroll
+  for (int x = 0; x < BS; ++x)
+#pragma unroll
+    for (int y = 0; y < BS; ++y) {
+      W[x][y] = d.gsum[(i0 + x) * RP + k0 + y];
+      T[x][y] = (i0 + x == k0 + y) ? 1.0 : 0.0;
+    }
+  if (bi == bk) {
+#pragma unroll
+    for (int x = 0; x < BS; ++x) sm.diag[i0 + x] = W[x][x];
+  }
+  __syncthreads();
+  if (t < kWave) {
+    // max of diag(G) over the first wave (max is order-independent)
+    double mx = 0.0;
+    int nonfinite = 0;
+    for (int j = t; j < RP; j += kWave) {
+      const double gv = sm.diag[j];
+      if (!isfinite(gv)) nonfinite = 1;
+      if (gv > mx) mx = gv;
+    }
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+      const double o = __shfl_xor(mx, off);
+      mx = o > mx ? o : mx;
+      nonfinite |= __shfl_xor(nonfinite, off);
+    }
+    if (t == 0) {
+      sm.thr = kPivotTol * mx;
+      if (nonfinite && flags) atomicOr(flags, FLAG_NONFINITE);
+    }
+  }
+  __syncthreads();
+  const double thr = sm.thr;
+
+#pragma unroll 1
+  for (int j = 0; j < RP; ++j) {
+    const int buf = j & 1;
+    const int jb = j / BS, jx = j % BS;
+    // (selects instead of W[jx] / T[.][jx]: register arrays need
+    // compile-time indices)
+    if (bi == jb) {
+#pragma unroll
+      for (int y = 0; y < BS; ++y) {
+        double w = W[0][y];
+#pragma unroll
+        for (int xx = 1; xx < BS; ++xx) w = (jx == xx) ? W[xx][y] : w;
+        sm.roww[buf][k0 + y] = w;
+      }
+    }
+    if (bk == jb) {
+#pragma unroll
+      for (int x = 0; x < BS; ++x) {
+        double v = T[x][0];
+#pragma unroll
+        for (int yy = 1; yy < BS; ++yy) v = (jx == yy) ? T[x][yy] : v;
+        sm.colt[buf][i0 + x] = v;
+      }
+    }
+    __syncthreads();
+    const double piv = sm.roww[buf][j];
+    const bool dep = (j >= r) || (piv <= thr);
+    if (!dep) {
+      const double ip = 1.0 / piv;
+      double ci[BS], cl[BS];
+#pragma unroll
+      for (int x = 0; x < BS; ++x) {
+        ci[x] = sm.roww[buf][i0 + x] * ip;
+        cl[x] = sm.colt[buf][i0 + x] * ip;
+      }
+#pragma unroll
+      for (int y = 0; y < BS; ++y) {
+        const int k = k0 + y;
+        if (k > j) {
+          const double wk = sm.roww[buf][k];
+#pragma unroll
+          for (int x = 0; x < BS; ++x) {
+            const int i = i0 + x;
+            if (i > j) {
+              if (i <= k) W[x][y] = fma(-ci[x], wk, W[x][y]);
+            } else {
+              T[x][y] = fma(-cl[x], wk, T[x][y]);
+            }
+          }
+        }
+      }
+    }
+    if (t == 0) {
+      sm.diag[j] = dep ? 0.0 : sqrt(piv);
+      sm.dep[j] = dep ? 1 : 0;
+      if (dep && j < r && flags) atomicOr(flags, FLAG_RANK_DEFICIENT);
+    }
+  }
+  __syncthreads();
+
+  double* out = MODE == 0 ? d.t1 : d.tm;
+#pragma unroll
+  for (int x = 0; x < BS; ++x)
+#pragma unroll
+    for (int y = 0; y < BS; ++y) {
+      const int l = i0 + x, k = k0 + y;
+      double v = 0.0;
+      if (l <= k && !sm.dep[k]) v = T[x][y] / sm.diag[k];
+      out[l * RP + k] = v;
+    }
+  if (MODE == 0 && t < kWave) {
+    double dmax = 0.0, dmin = 1e308;
+    for (int j = t; j < r; j += kWave) {
+      if (sm.dep[j]) continue;
+      const double v = sm.diag[j];
+      dmax = v > dmax ? v : dmax;
+      dmin = v < dmin ? v : dmin;
+    }
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+      const double a = __shfl_xor(dmax, off), c = __shfl_xor(dmin, off);
+      dmax = a > dmax ? a : dmax;
+      dmin = c < dmin ? c : dmin;
+    }
+    if (t == 0) d.info[0] = (dmax > 0.0 && dmax > kSecondPassCond * dmin) ? 1u : 0u;
+  }
+}
+
+template <int RP, int MODE>
+__global__ __launch_bounds__(LC_THREADS) void k_lchol(OCC_KARGS, uint32_t* flags) {
+  __shared__ LCSmem<RP> sm;
+  if (count == 1) lchol_body<RP, MODE>(single, flags, sm);
+  else lchol_body<RP, MODE>(table[blockIdx.x], flags, sm);
+}
+
+// -------------------------------------------------------------------------
+// k_lapply: P_hat = S T for 128 rows, S = praw, T = t1 (MODE 0) or, in the
+// second pass, S = the first pass's P_hat, T = tm (in place).  fp64
+// arithmetic, fp32 result.  Thread (rb, cb) computes rows 4rb..4rb+3,
+// columns RP/32*cb.. of a 32-row chunk.  The final P_hat (no second pass
+// pending) also goes to the caller's P and, transposed, to phat_t.
+// -------------------------------------------------------------------------
+template <int RP>
+struct LASmem {
+  double T[RP * RP];
+  float src[32][RP + 4];
+};
+
+template <int RP, int MODE>
+__device__ __forceinline__ void la_body(const Desc& d, int b, LASmem<RP>& sm) {
+  const uint32_t need = d.info[0];
+  if (MODE == 1 && !need) return;
+  const bool fin = (MODE == 1) || !need;
+  const double* Tg = MODE == 0 ? d.t1 : d.tm;
+  const float* src = MODE == 0 ? d.praw : d.phat;
+  constexpr int CB = RP / 32;
+  const int t = threadIdx.x, rb = t >> 5, cb = t & 31;
+  for (int idx = t; idx < RP * RP; idx += kBlock) sm.T[idx] = Tg[idx];
+  const int r_lo = b * L_AROWS, r_hi = min(d.m, r_lo + L_AROWS);
+  for (int c0 = r_lo; c0 < r_hi; c0 += 32) {
+    for (int idx = t; idx < 32 * RP; idx += kBlock) {
+      const int i = idx / RP, k = idx % RP;
+      sm.src[i][k] = (c0 + i < r_hi) ? src[(int64_t)(c0 + i) * RP + k] : 0.f;
+    }
+    __syncthreads();
+    double acc[4][CB];
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+      for (int y = 0; y < CB; ++y) acc[x][y] = 0.0;
+    for (int l = 0; l < RP; ++l) {
+      double sv[4], tv[CB];
+#pragma unroll
+      for (int x = 0; x < 4; ++x) sv[x] = (double)sm.src[4 * rb + x][l];
+#pragma unroll
+      for (int y = 0; y < CB; ++y) tv[y] = sm.T[l * RP + CB * cb + y];
+#pragma unroll
+      for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < CB; ++y) acc[x][y] = fma(sv[x], tv[y], acc[x][y]);
+    }
+    float o[4][CB];
+#pragma unroll
+    for (int x = 0; x < 4; ++x)
+#pragma unroll
+      for (int y = 0; y < CB; ++y) o[x][y] = (float)acc[x][y];
+#pragma unroll
+    for (int x = 0; x < 4; ++x) {
+      const int row = c0 + 4 * rb + x;
+      if (row < r_hi) {
+        st_f<CB>(d.phat + (int64_t)row * RP + CB * cb, o[x]);
+        if (fin) {
+#pragma unroll
+          for (int y = 0; y < CB; ++y) {
+            const int k = CB * cb + y;
+            if (k < d.r) d.P[(int64_t)row * d.r + k] = o[x][y];
+          }
+        }
+      }
+    }
+    if (fin) {
+      // rows past m carry zeros (their source rows were staged as 0)
+#pragma unroll
+      for (int y = 0; y < CB; ++y) {
+        const int k = CB * cb + y;
+        *(float4*)(d.phat_t + (int64_t)k * d.m_pad + c0 + 4 * rb) =
+            make_float4(o[0][y], o[1][y], o[2][y], o[3][y]);
+      }
+    }
+    __syncthreads();
+  }
+}
+
+template <int RP, int MODE>
+__global__ __launch_bounds__(kBlock) void k_lapply(OCC_KARGS) {
+  __shared__ __attribute__((aligned(16))) LASmem<RP> sm;
+#define B_(d, b) la_body<RP, MODE>(d, b, sm)
+  OCC_DISPATCH(K_APPLY, B_)
+#undef B_
+}
+
+// -------------------------------------------------------------------------
+// k_lq: Q partials = A^T P_hat for one column tile and one row split.
+// Lane (g, li) of wave w loads lq_cpl columns starting at
+// ct*BC + 32*cpl*w + cpl*li of rows 2ks + g; MFMA tile t of rank tile u then
+// holds Q[col = base + cpl*i + t][rank = NU*j + u].
+// -------------------------------------------------------------------------
+template <int RP>
+struct LQSmem {
+  float p[2][L_QG][RP + 4];
+};
+
+template <int DT, int RP, int SA>
+__device__ __forceinline__ void lq_body(const Desc& d, int b, LQSmem<RP>& sm) {
+  constexpr int NU = RP / 32, CPL = lq_cpl(RP), BC = lq_block_cols(RP);
+  constexpr int PF = L_QG * RP / 4;   // float4s of one P_hat stage
+  static_assert(PF <= kBlock, "one float4 per thread per stage");
+  const bool vec = d.vec != 0;
+  const int wave = wave_id(), lane = threadIdx.x & 63;
+  const int li = lane & 31, g = lane >> 5;
+  const int t = threadIdx.x;
+  const int col_tiles = (d.n + BC - 1) / BC;
+  const int ct = b % col_tiles, s = b / col_tiles;
+  const int cw = ct * BC + wave * 32 * CPL;
+  const int col = cw + CPL * li;
+  const int r_lo = s * d.q_rows, r_hi = min(d.m, r_lo + d.q_rows);
+  const int ngrp = (r_hi - r_lo + L_QG - 1) / L_QG;
+  const int pi = (4 * t) / RP, pk = (4 * t) % RP;   // this thread's staging slot
+
+  f16v acc[CPL][NU];
+#pragma unroll
+  for (int x = 0; x < CPL; ++x)
+#pragma unroll
+    for (int u = 0; u < NU; ++u) acc[x][u] = f16v{};
+
+  f4v pr = f4v{0.f, 0.f, 0.f, 0.f};
+  if (t < PF) {
+    const int row = r_lo + pi;
+    if (row < r_hi) pr = *(const f4v*)(d.phat + (int64_t)row * RP + pk);
+    *(f4v*)(&sm.p[0][pi][pk]) = pr;
+  }
+  RawA<DT, SA, CPL> cur[4], nxt[4];
+#pragma unroll
+  for (int ks = 0; ks < 4; ++ks) {
+    const int row = r_lo + 2 * ks + g;
+    cur[ks] = rawa_load<DT, SA, CPL>(d, vec, row < r_hi ? row : d.m, col, d.n);
+  }
+  __syncthreads();
+
+  for (int grp = 0; grp < ngrp; ++grp) {
+    const bool more = grp + 1 < ngrp;
+    const int rn = r_lo + L_QG * (grp + 1);
+    if (more) {
+      if (t < PF) {
+        const int row = rn + pi;
+        pr = row < r_hi ? *(const f4v*)(d.phat + (int64_t)row * RP + pk) : f4v{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const int row = rn + 2 * ks + g;
+        nxt[ks] = rawa_load<DT, SA, CPL>(d, vec, row < r_hi ? row : d.m, col, d.n);
+      }
+    }
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      float bv[NU];
+      ld_f<NU>(&sm.p[grp & 1][2 * ks + g][NU * li], bv);
+#pragma unroll
+      for (int x = 0; x < CPL; ++x) {
+        const float a = rawa_val<DT, SA, CPL>(cur[ks], x);
+#pragma unroll
+        for (int u = 0; u < NU; ++u) acc[x][u] = mfma32(a, bv[u], acc[x][u]);
+      }
+    }
+    if (more) {
+      if (t < PF) *(f4v*)(&sm.p[(grp + 1) & 1][pi][pk]) = pr;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) cur[ks] = nxt[ks];
+    }
+    __syncthreads();
+  }
+
+#pragma unroll
+  for (int x = 0; x < CPL; ++x)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int c = cw + CPL * mf32_row(v, g) + x;
+      if (c < d.n) {
+        float o[NU];
+#pragma unroll
+        for (int u = 0; u < NU; ++u) o[u] = acc[x][u][v];
+        st_f<NU>(d.qpart + ((int64_t)s * d.n + c) * RP + NU * li, o);
+      }
+    }
+}
+
+template <int DT, int RP, int SA>
+__global__ __launch_bounds__(kBlock) void k_lq(OCC_KARGS) {
+  __shared__ __attribute__((aligned(16))) LQSmem<RP> sm;
+#define B_(d, b) lq_body<DT, RP, SA>(d, b, sm)
+  OCC_DISPATCH(K_PASS_Q, B_)
+#undef B_
+}
+
+// -------------------------------------------------------------------------
+// k_ml: M_hat = P_hat Q^T, err = A - M_hat for one column tile and d.mr rows.
+// SRC 0: P_hat from phat_t, Q from qpad (fused step).  SRC 1: the caller's P
+// (m x r) and Q (n x r), zero past rank r (stand-alone decompression; the
+// same products, so both give bitwise the same M_hat).
+// -------------------------------------------------------------------------
+template <int RP>
+struct LMSmem {
+  float p[2][RP][32];   // P_hat tile, transposed: [rank][row]
+};
+
+template <int RP, int SRC>
+__device__ __forceinline__ void lm_stage_direct(const Desc& d, int row0, float (*dst)[32]) {
+  for (int idx = threadIdx.x; idx < RP * 32; idx += kBlock) {
+    const int k = idx >> 5, i = idx & 31;
+    const int row = row0 + i;
+    dst[k][i] = (row < d.m && k < d.r) ? d.P[(int64_t)row * d.r + k] : 0.f;
+  }
+}
+
+template <int DT, int RP, int SA, int SRC, bool WM, bool WE>
+__device__ __forceinline__ void lm_body(const Desc& d, int b, LMSmem<RP>& sm) {
+  constexpr int NCT = lm_tiles(RP), KP = RP / 2, BC = lm_block_cols(RP);
+  constexpr int SF = RP * 8 / kBlock;   // float4s per thread per P_hat tile
+  const int wave = wave_id(), lane = threadIdx.x & 63;
+  const int li = lane & 31, g = lane >> 5;
+  const int t = threadIdx.x;
+  const int col_tiles = (d.n + BC - 1) / BC;
+  const int ct = b % col_tiles, rb = b / col_tiles;
+  const int r_lo = rb * d.mr, r_hi = min(d.m, r_lo + d.mr);
+  const int ntile = (r_hi - r_lo + 31) / 32;
+  const int cw = ct * BC + wave * 32 * NCT;
+
+  float qv[NCT][KP];
+#pragma unroll
+  for (int c = 0; c < NCT; ++c) {
+    const int col = cw + 32 * c + li;
+#pragma unroll
+    for (int kp = 0; kp < KP; ++kp) {
+      const int k = 2 * kp + g;
+      float v = 0.f;
+      if (SRC == 0) {
+        if (col < d.n_pad) v = d.qpad[(int64_t)col * RP + k];
+      } else {
+        if (col < d.n && k < d.r) v = d.Q[(int64_t)col * d.r + k];
+      }
+      qv[c][kp] = v;
+    }
+  }
+
+  f4v pr[SF > 0 ? SF : 1];
+  if (SRC == 0) {
+#pragma unroll
+    for (int x = 0; x < SF; ++x) {
+      const int f = t + kBlock * x, k = f >> 3, part = f & 7;
+      pr[x] = *(const f4v*)(d.phat_t + (int64_t)k * d.m_pad + r_lo + 4 * part);
+      *(f4v*)(&sm.p[0][k][4 * part]) = pr[x];
+    }
+  } else {
+    lm_stage_direct<RP, SRC>(d, r_lo, sm.p[0]);
+  }
+  __syncthreads();
+
+  for (int tile = 0; tile < ntile; ++tile) {
+    const int row0 = r_lo + 32 * tile;
+    const bool more = tile + 1 < ntile;
+    if (SRC == 0 && more) {
+#pragma unroll
+      for (int x = 0; x < SF; ++x) {
+        const int f = t + kBlock * x, k = f >> 3, part = f & 7;
+        pr[x] = *(const f4v*)(d.phat_t + (int64_t)k * d.m_pad + row0 + 32 + 4 * part);
+      }
+    }
+    // A for this tile's outputs (issued before the products to hide latency)
+    RawA<DT, SA, 1> av[NCT][16];
+    if (WE) {
+#pragma unroll
+      for (int c = 0; c < NCT; ++c)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          av[c][v] = rawa_load<DT, SA, 1>(d, true, row0 + mf32_row(v, g), cw + 32 * c + li, d.n);
+    }
+    f16v acc[NCT];
+#pragma unroll
+    for (int c = 0; c < NCT; ++c) acc[c] = f16v{};
+    const float* pa = &sm.p[tile & 1][g][li];
+#pragma unroll
+    for (int kp = 0; kp < KP; ++kp) {
+      const float a = pa[2 * kp * 32];
+#pragma unroll
+      for (int c = 0; c < NCT; ++c) acc[c] = mfma32(a, qv[c][kp], acc[c]);
+    }
+#pragma unroll
+    for (int c = 0; c < NCT; ++c) {
+      const int col = cw + 32 * c + li;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = row0 + mf32_row(v, g);
+        if (row < r_hi && col < d.n) {
+          const float mh = acc[c][v];
+          if (WM) __builtin_nontemporal_store(mh, d.Mhat + (int64_t)row * d.ldh + col);
+          if (WE) {
+            const float e = rawa_val<DT, SA, 1>(av[c][v], 0) - mh;
+            __builtin_nontemporal_store(e, d.err_out + (int64_t)row * d.lde_out + col);
+          }
+        }
+      }
+    }
+    if (more) {
+      if (SRC == 0) {
+#pragma unroll
+        for (int x = 0; x < SF; ++x) {
+          const int f = t + kBlock * x, k = f >> 3, part = f & 7;
+          *(f4v*)(&sm.p[(tile + 1) & 1][k][4 * part]) = pr[x];
+        }
+      } else {
+        lm_stage_direct<RP, SRC>(d, row0 + 32, sm.p[(tile + 1) & 1]);
+      }
+    }
+    __syncthreads();
+  }
+}
+
+template <int DT, int RP, int SA, int SRC, bool WM, bool WE>
+__global__ __launch_bounds__(kBlock) void k_ml(OCC_KARGS) {
+  __shared__ __attribute__((aligned(16))) LMSmem<RP> sm;
+#define B_(d, b) lm_body<DT, RP, SA, SRC, WM, WE>(d, b, sm)
+  OCC_DISPATCH(K_MHAT, B_)
+#undef B_
+}
+
+}  // namespace occ

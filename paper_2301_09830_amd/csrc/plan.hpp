@@ -30,16 +30,12 @@ enum Kind : int {
   K_NUM
 };
 
-// Tile constants of the small-rank vector-ALU path.
-constexpr int PP_ROWS = 64;     // pass P: rows per block (one lane per row)
-constexpr int PP_SUB = 32;      // pass P: columns per wave sub-tile
-constexpr int PP_PITCH = 36;    // pass P: LDS row pitch in floats
-constexpr int G_ROWS = 256;     // Gram partial: rows per block
-constexpr int MH_ROWS = 64;     // M_hat pass: rows per block
+// Tile constants of the stand-alone reconstruction kernel (k_mhat, used by
+// occ_decompress at padded rank <= 16).
+constexpr int MH_ROWS = 64;     // rows per block
 
-// Rank chunk and columns per lane of the streaming kernels for a padded rank.
+// Columns per lane of k_mhat.
 __host__ __device__ constexpr int cols_per_lane(int rp) { return rp <= 16 ? 4 : 1; }
-__host__ __device__ constexpr int q_rank_chunk(int rp) { return rp <= 16 ? rp : 32; }
 
 struct Desc {
   // caller buffers
@@ -56,32 +52,34 @@ struct Desc {
   float* ppart;          // sp x m x rp
   float* qpart;          // sq x n x rp
   double* gpart;         // ng x rp x rp
-  double* gsub;          // ceil(ng / 16) x rp x rp (group sums of the Gram tree)
   double* gsum;          // rp x rp
   double* t1;            // rp x rp
-  double* tm;            // rp x rp
+  double* tm;            // rp x rp (large-rank path: T2 of the second pass)
   uint32_t* info;        // [0] = second CholeskyQR pass needed
+  float* phat_t;         // large-rank path: P_hat transposed, rp x m_pad
   // shapes
   int32_t m, n, r;
   int32_t ldm, lde_in, lde_out, ldh;
   int32_t n_pad;
-  int32_t sp, p_cols;    // pass P: column splits and columns per split (multiple of PP_SUB)
-  int32_t ng;            // Gram partial blocks (G_ROWS rows each)
-  int32_t sq, q_rows;    // pass Q: row splits and rows per split
-  int32_t gb;            // fused path: blocks of the Gram-sum/Cholesky kernel
+  int32_t sp, p_cols;    // left product: column splits and columns per split (multiple of 32)
+  int32_t ng;            // Gram partials (one per block of the Gram kernel)
+  int32_t sq, q_rows;    // right product: row splits and rows per split
   int32_t blk[K_NUM];    // first block of this matrix in each kernel's grid
-  int32_t fused;         // 1: fused small-rank path (rank padded to <= 16)
-  int32_t pad_;
+  int32_t fused;         // 1: small-rank path (rank padded to <= 16)
+  int32_t m_pad;         // large-rank path: rows of phat_t (multiple of 32)
+  int32_t mr;            // large-rank path: rows per block of the reconstruction pass
+  int32_t vec;           // large-rank path: 16-byte vector loads allowed
 };
 
 // Tiling of one matrix (host side).
 struct Tiling {
-  int sp, p_cols, ng, sq, q_rows, n_pad, gb;
+  int sp, p_cols, ng, sq, q_rows, n_pad, m_pad, mr;
   int64_t blocks[K_NUM];
 };
 
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline int64_t round_up(int64_t a, int64_t b) { return cdiv(a, b) * b; }
+inline int64_t clamp64(int64_t v, int64_t lo, int64_t hi) { return v < lo ? lo : (v > hi ? hi : v); }
 
 inline int padded_rank(int r) {
   int p = 4;
@@ -89,75 +87,86 @@ inline int padded_rank(int r) {
   return p;
 }
 
-// Fused small-rank path: tile constants shared with kernels_small.hpp.
+// Small-rank path (padded rank <= 16): tile constants shared with
+// kernels_small.hpp and kernels_mfma16.hpp.
 constexpr int kFusedMaxRank = 16;
 constexpr int F_PROWS = 32;       // left product: rows per block
 constexpr int F_QCOLS = 128;      // right product: columns per block
-constexpr int F_QMAXROWS = 512;   // right product: rows per block (P_hat rows in LDS)
 constexpr int F_MHROWS = 256;     // reconstruction: rows per block
 constexpr int F_MHCOLS = 256;     // reconstruction: columns per block (4 per lane)
 constexpr int F_QBLOCKS = 512;    // right product: target number of blocks
 constexpr int F_ORTHROWS = 128;   // Cholesky/P_hat kernel: rows of P_hat per block
 
-inline Tiling make_tiling(int64_t m, int64_t n, int rp, bool fused) {
+// Large-rank path (padded rank 32, 64, 128): tile constants shared with
+// kernels_large.hpp.
+constexpr int L_PROWS = 128;      // left product: rows per block (4 waves x 32)
+constexpr int L_KC = 32;          // left product: columns per K-step
+constexpr int L_GROWS = 256;      // Gram partials: rows per block
+constexpr int L_AROWS = 128;      // P_hat = P T: rows per block
+constexpr int L_QG = 8;           // right product: rows per LDS stage
+// right product: columns per lane and per block
+__host__ __device__ constexpr int lq_cpl(int rp) { return rp >= 128 ? 1 : 128 / rp; }
+__host__ __device__ constexpr int lq_block_cols(int rp) { return 128 * lq_cpl(rp); }
+// reconstruction: 32-column MFMA tiles per wave and columns per block
+__host__ __device__ constexpr int lm_tiles(int rp) { return rp >= 64 ? 1 : 2; }
+__host__ __device__ constexpr int lm_block_cols(int rp) { return 128 * lm_tiles(rp); }
+
+inline Tiling make_tiling(int64_t m, int64_t n, int rp) {
   Tiling t{};
-  t.n_pad = (int)round_up(n, PP_SUB);
-  // pass P: 64-row tiles; split the columns until there are enough blocks,
-  // keeping at least 128 (fused: 256) columns per split.
-  int64_t row_tiles = cdiv(m, PP_ROWS);
-  const int64_t p_blocks = fused ? cdiv(m, F_PROWS) : row_tiles;
-  int64_t sp = cdiv(1024, p_blocks);
-  int64_t max_sp = cdiv(n, fused ? 256 : 128);
-  if (sp > max_sp) sp = max_sp;
-  if (sp < 1) sp = 1;
-  t.p_cols = (int)round_up(cdiv(n, sp), PP_SUB);
-  t.sp = (int)cdiv(n, t.p_cols);
-  t.ng = fused ? (int)p_blocks : (int)cdiv(m, G_ROWS);
-  if (fused) {
+  t.n_pad = (int)round_up(n, 32);
+  t.m_pad = (int)round_up(m, 32);
+  if (rp <= kFusedMaxRank) {
     // left product: whole rows per block, no column splits
+    const int64_t p_blocks = cdiv(m, F_PROWS);
     t.sp = 1;
-    t.p_cols = (int)round_up(n, PP_SUB);
+    t.p_cols = (int)round_up(n, 32);
     t.ng = (int)p_blocks;
-    t.gb = 1;
     const int64_t col_tiles = cdiv(n, F_QCOLS);
-    int64_t sq = cdiv(F_QBLOCKS, col_tiles);
-    const int64_t max_sq = cdiv(m, 32);
-    if (sq > max_sq) sq = max_sq;
-    if (sq < 1) sq = 1;
+    const int64_t sq = clamp64(cdiv(F_QBLOCKS, col_tiles), 1, cdiv(m, 32));
     t.q_rows = (int)round_up(cdiv(m, sq), 4);
     t.sq = (int)cdiv(m, t.q_rows);
+    t.mr = 0;
     t.blocks[K_QPAD] = cdiv((int64_t)t.n_pad * rp, kBlock);
     t.blocks[K_PASS_P] = p_blocks;
     t.blocks[K_PGRAM] = cdiv(m, F_ORTHROWS);
-    t.blocks[K_GSUM] = 0;
-    t.blocks[K_GRAM2] = 0;
-    t.blocks[K_APPLY] = 0;
     t.blocks[K_PASS_Q] = col_tiles * t.sq;
     t.blocks[K_QRED] = cdiv(n * rp, kBlock);
     t.blocks[K_MHAT] = cdiv(n, F_MHCOLS) * cdiv(m, F_MHROWS);
     return t;
   }
-  // pass Q: column tiles of 64*cols_per_lane; row splits up to ~1024 blocks
-  int cpl = cols_per_lane(rp);
-  int64_t col_tiles = cdiv(n, (int64_t)kWave * cpl);
-  int rchunks = rp / q_rank_chunk(rp);
-  int64_t sq = cdiv(1024, col_tiles * rchunks);
-  int64_t max_sq = cdiv(m, 64);
-  if (sq > max_sq) sq = max_sq;
-  if (sq < 1) sq = 1;
-  t.q_rows = (int)round_up(cdiv(m, sq), 4);
+  // left product: 128-row tiles; split the columns (>= 1024 per split) until
+  // a matrix has about 256 blocks
+  const int64_t row_tiles = cdiv(m, L_PROWS);
+  const int64_t sp = clamp64(cdiv(256, row_tiles), 1, cdiv(n, 1024));
+  t.p_cols = (int)round_up(cdiv(n, sp), L_KC);
+  t.sp = (int)cdiv(n, t.p_cols);
+  t.ng = (int)cdiv(m, L_GROWS);
+  // right product: column tiles, rows split (>= 1024 per split) to about
+  // 256 blocks
+  const int64_t ctq = cdiv(n, lq_block_cols(rp));
+  const int64_t sq = clamp64(cdiv(256, ctq), 1, cdiv(m, 1024));
+  t.q_rows = (int)round_up(cdiv(m, sq), L_QG);
   t.sq = (int)cdiv(m, t.q_rows);
-
+  // reconstruction: column tiles x row blocks (multiple of 32 rows), about
+  // 512 blocks
+  const int64_t ctm = cdiv(n, lm_block_cols(rp));
+  const int64_t rbm = clamp64(cdiv(512, ctm), 1, cdiv(m, 32));
+  t.mr = (int)round_up(cdiv(m, rbm), 32);
   t.blocks[K_QPAD] = cdiv((int64_t)t.n_pad * rp, kBlock);
   t.blocks[K_PASS_P] = row_tiles * t.sp;
   t.blocks[K_PGRAM] = t.ng;
   t.blocks[K_GSUM] = cdiv((int64_t)rp * rp, kBlock);
   t.blocks[K_GRAM2] = t.ng;
-  t.blocks[K_APPLY] = cdiv(m, 64);
-  t.blocks[K_PASS_Q] = col_tiles * t.sq * rchunks;
+  t.blocks[K_APPLY] = cdiv(m, L_AROWS);
+  t.blocks[K_PASS_Q] = ctq * t.sq;
   t.blocks[K_QRED] = cdiv(n * rp, kBlock);
-  t.blocks[K_MHAT] = cdiv(n, (int64_t)kWave * cpl) * cdiv(m, MH_ROWS);
+  t.blocks[K_MHAT] = ctm * cdiv(m, t.mr);
   return t;
+}
+
+// Grid of k_mhat (stand-alone reconstruction at padded rank <= 16).
+inline int64_t mhat_blocks(int64_t m, int64_t n, int rp) {
+  return cdiv(n, (int64_t)kWave * cols_per_lane(rp)) * cdiv(m, MH_ROWS);
 }
 
 // Workspace layout: [header 256 B: sticky flags word][descriptor table]
@@ -168,7 +177,7 @@ constexpr size_t kAlign = 256;
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Regions {
-  size_t qpad, phat, praw, ppart, qpart, gpart, gsub, gsum, t1, tm, info, total;
+  size_t qpad, phat, praw, ppart, qpart, gpart, gsum, t1, tm, info, phat_t, total;
 };
 
 inline Regions matrix_regions(int64_t m, int64_t n, int rp, const Tiling& t) {
@@ -181,11 +190,11 @@ inline Regions matrix_regions(int64_t m, int64_t n, int rp, const Tiling& t) {
   g.ppart = take((size_t)t.sp * m * rp * 4);
   g.qpart = take((size_t)t.sq * n * rp * 4);
   g.gpart = take((size_t)t.ng * rp * rp * 8);
-  g.gsub = take((size_t)(t.gb > 0 ? t.gb : cdiv(t.ng, 16)) * rp * rp * 8);
   g.gsum = take((size_t)rp * rp * 8);
   g.t1 = take((size_t)rp * rp * 8);
   g.tm = take((size_t)rp * rp * 8);
   g.info = take(64);
+  g.phat_t = take(rp > kFusedMaxRank ? (size_t)rp * t.m_pad * 4 : 0);
   g.total = off;
   return g;
 }

@@ -11,7 +11,7 @@ pytestmark = pytest.mark.gpu
 
 
 def _inputs(m=513, n=300, rank=16, dtype="bf16", seed=5):
-    w = WORKLOADS[2].scaled([(m, n)], rank=rank)
+    w = WORKLOADS[2].scaled([(m, n)], rank=rank, m_dtype=dtype)
     M = w.matrix(seed, 0)
     return w, M, w.q0(0)
 
@@ -23,18 +23,23 @@ def _run_step(M_dev, err, Q, rank, iters, flags_write=True):
     return P, Mh
 
 
-def test_invariants_fp32_level():
+# Ranks on both kernel paths: padded rank <= 16 and padded rank 32..128.
+SMALL_LARGE = [16, 64]
+
+
+@pytest.mark.parametrize("rank", SMALL_LARGE + [128])
+def test_invariants_fp32_level(rank):
     torch = torch_mod()
-    w, M, q0 = _inputs()
+    w, M, q0 = _inputs(rank=rank)
     Md = to_device(M, "bf16")
     err0 = torch.randn(M.shape, device="cuda") * 0.01
     err = err0.clone()
     Q = torch.from_numpy(q0).cuda()
-    P, Mh = _run_step(Md, err, Q, 16, 1)
+    P, Mh = _run_step(Md, err, Q, rank, 1)
     A = Md.float() + err0
     Pd = P.double()
     eye = Pd.T @ Pd
-    assert torch.allclose(eye, torch.eye(16, dtype=torch.float64, device="cuda"), atol=1e-5)
+    assert torch.allclose(eye, torch.eye(rank, dtype=torch.float64, device="cuda"), atol=1e-5)
     # conservation: M_hat + err_new == A up to one fp32 rounding of err
     diff = (Mh.double() + err.double() - A.double()).abs().max().item()
     assert diff <= 2 * np.finfo(np.float32).eps * A.abs().max().item()
@@ -43,17 +48,21 @@ def test_invariants_fp32_level():
     assert ortho <= 1e-4 * err.double().norm().item()
 
 
-def test_fused_equals_unfused_bitwise():
+@pytest.mark.parametrize("rank,dtype", [(12, "bf16"), (40, "bf16"), (100, "f32")])
+def test_fused_equals_unfused_bitwise(rank, dtype):
+    """occ_step (large ranks: A stored over err, later passes read it back)
+    equals occ_compress (re-reads M + err_prev) + occ_decompress +
+    occ_err_update bit for bit."""
     from paper_2301_09830_amd import optcc
     torch = torch_mod()
-    w, M, q0 = _inputs(m=700, n=260, rank=12)
-    Md = to_device(M, "bf16")
+    w, M, q0 = _inputs(m=700, n=260, rank=rank, dtype=dtype)
+    Md = to_device(M, dtype)
     err = torch.randn(M.shape, device="cuda") * 0.02
     err_a, err_b = err.clone(), err.clone()
     Qa = torch.from_numpy(q0).cuda()
     Qb = Qa.clone()
-    P1, Mh1 = optcc.occ_step(Md, err_a, Qa, 12, 2)
-    P2 = optcc.occ_compress(Md, err_b, Qb, 12, 2)
+    P1, Mh1 = optcc.occ_step(Md, err_a, Qa, rank, 2)
+    P2 = optcc.occ_compress(Md, err_b, Qb, rank, 2)
     Mh2 = optcc.occ_decompress(P2, Qb)
     optcc.occ_err_update(Md, err_b, Mh2, err_new=err_b)
     torch.cuda.synchronize()
@@ -61,108 +70,114 @@ def test_fused_equals_unfused_bitwise():
         assert torch.equal(x.view(torch.int32), y.view(torch.int32))
 
 
-def test_compress_without_error_buffer():
+@pytest.mark.parametrize("rank", [8, 64])
+def test_compress_without_error_buffer(rank):
     from paper_2301_09830_amd import optcc
     torch = torch_mod()
-    w, M, q0 = _inputs(m=300, n=200, rank=8)
+    w, M, q0 = _inputs(m=300, n=200, rank=rank)
     Md = to_device(M, "bf16")
     Qa = torch.from_numpy(q0).cuda()
     Qb = Qa.clone()
     zero = torch.zeros(M.shape, device="cuda")
-    Pa = optcc.occ_compress(Md, None, Qa, 8, 1)
-    Pb = optcc.occ_compress(Md, zero, Qb, 8, 1)
+    Pa = optcc.occ_compress(Md, None, Qa, rank, 1)
+    Pb = optcc.occ_compress(Md, zero, Qb, rank, 1)
     torch.cuda.synchronize()
     assert torch.equal(Pa, Pb) and torch.equal(Qa, Qb)
 
 
-def test_batched_equals_single_bitwise():
+@pytest.mark.parametrize("rank", [16, 48])
+def test_batched_equals_single_bitwise(rank):
     from paper_2301_09830_amd import optcc
     torch = torch_mod()
     shapes = [(300, 96), (96, 96), (400, 96), (96, 384), (77, 130)]
-    w = WORKLOADS[3].scaled(shapes, rank=16)
+    w = WORKLOADS[3].scaled(shapes, rank=rank)
     mats = [to_device(w.matrix(0, j), "f32") for j in range(len(shapes))]
     errs = [torch.randn(s, device="cuda") * 1e-3 for s in shapes]
     qs = [torch.from_numpy(w.q0(j)).cuda() for j in range(len(shapes))]
     single, batch = [], []
     for j, (m, n) in enumerate(shapes):
         e, q = errs[j].clone(), qs[j].clone()
-        P, Mh = optcc.occ_step(mats[j], e, q, 16, 2)
+        P, Mh = optcc.occ_step(mats[j], e, q, rank, 2)
         single.append((P, Mh, e, q))
     items = []
     for j, (m, n) in enumerate(shapes):
         items.append((mats[j], errs[j].clone(), qs[j].clone(),
-                      torch.empty((m, 16), device="cuda"), torch.empty((m, n), device="cuda")))
-    optcc.occ_step_batched(items, 16, 2)
+                      torch.empty((m, rank), device="cuda"), torch.empty((m, n), device="cuda")))
+    optcc.occ_step_batched(items, rank, 2)
     torch.cuda.synchronize()
     for (P, Mh, e, q), (_, eb, qb, Pb, Mhb) in zip(single, items):
         assert torch.equal(P, Pb) and torch.equal(Mh, Mhb) and torch.equal(e, eb) and torch.equal(q, qb)
 
 
-def test_deterministic_run_to_run():
+@pytest.mark.parametrize("rank", [16, 128])
+def test_deterministic_run_to_run(rank):
     from paper_2301_09830_amd import optcc
     torch = torch_mod()
-    w, M, q0 = _inputs(m=2048, n=1024, rank=16)
+    w, M, q0 = _inputs(m=2048, n=1024, rank=rank)
     Md = to_device(M, "bf16")
     outs = []
     for _ in range(2):
         err = torch.zeros(M.shape, device="cuda")
         Q = torch.from_numpy(q0).cuda()
         for _s in range(3):
-            P, Mh = optcc.occ_step(Md, err, Q, 16, 1)
+            P, Mh = optcc.occ_step(Md, err, Q, rank, 1)
         torch.cuda.synchronize()
         outs.append((P.clone(), Mh.clone(), err.clone(), Q.clone()))
     for x, y in zip(*outs):
         assert torch.equal(x, y)
 
 
-def test_resume_from_saved_state_bitwise():
+@pytest.mark.parametrize("rank", [16, 64])
+def test_resume_from_saved_state_bitwise(rank):
     from paper_2301_09830_amd import optcc
     torch = torch_mod()
-    w = WORKLOADS[2].scaled([(640, 384)])
+    w = WORKLOADS[2].scaled([(640, 384)], rank=rank)
     Ms = [to_device(w.matrix(s, 0), "bf16") for s in range(6)]
     err = torch.zeros((640, 384), device="cuda")
     Q = torch.from_numpy(w.q0(0)).cuda()
     for s in range(6):
-        optcc.occ_step(Ms[s], err, Q, 16, 1)
+        optcc.occ_step(Ms[s], err, Q, rank, 1)
     torch.cuda.synchronize()
     ref = (err.clone(), Q.clone())
     err = torch.zeros((640, 384), device="cuda")
     Q = torch.from_numpy(w.q0(0)).cuda()
     for s in range(3):
-        optcc.occ_step(Ms[s], err, Q, 16, 1)
+        optcc.occ_step(Ms[s], err, Q, rank, 1)
     saved = (err.cpu().numpy().copy(), Q.cpu().numpy().copy())     # checkpoint
     err = torch.from_numpy(saved[0]).cuda()
     Q = torch.from_numpy(saved[1]).cuda()
     for s in range(3, 6):
-        optcc.occ_step(Ms[s], err, Q, 16, 1)
+        optcc.occ_step(Ms[s], err, Q, rank, 1)
     torch.cuda.synchronize()
     assert torch.equal(err, ref[0]) and torch.equal(Q, ref[1])
 
 
-def test_no_mhat_flag_matches_full_step():
+@pytest.mark.parametrize("rank", SMALL_LARGE)
+def test_no_mhat_flag_matches_full_step(rank):
     from paper_2301_09830_amd import optcc
     torch = torch_mod()
-    w, M, q0 = _inputs(m=500, n=260, rank=16)
+    w, M, q0 = _inputs(m=500, n=260, rank=rank)
     Md = to_device(M, "bf16")
     e1 = torch.zeros(M.shape, device="cuda")
     e2 = e1.clone()
     q1 = torch.from_numpy(q0).cuda()
     q2 = q1.clone()
-    P1, _ = optcc.occ_step(Md, e1, q1, 16, 1)
-    P2, Mh2 = optcc.occ_step(Md, e2, q2, 16, 1, write_mhat=False)
+    P1, _ = optcc.occ_step(Md, e1, q1, rank, 1)
+    P2, Mh2 = optcc.occ_step(Md, e2, q2, rank, 1, write_mhat=False)
     torch.cuda.synchronize()
     assert Mh2 is None
     assert torch.equal(e1, e2) and torch.equal(P1, P2) and torch.equal(q1, q2)
 
 
-def test_zero_input_sets_rank_deficient_flag():
+@pytest.mark.parametrize("rank", [8, 64])
+def test_zero_input_sets_rank_deficient_flag(rank):
     from paper_2301_09830_amd import optcc
     torch = torch_mod()
     M = torch.zeros((200, 100), device="cuda")
     err = torch.zeros_like(M)
-    Q = torch.randn((100, 8), device="cuda")
-    ws = optcc.alloc_workspace(optcc.occ_workspace_bytes([(200, 100)], 8, 1))
-    P, Mh = optcc.occ_step(M, err, Q, 8, 1, ws=ws)
+    Q = torch.randn((100, rank), device="cuda")
+    ws = optcc.alloc_workspace(optcc.occ_workspace_bytes([(200, 100)], rank, 1))
+    P, Mh = optcc.occ_step(M, err, Q, rank, 1, ws=ws)
     flags = optcc.occ_get_flags(ws, clear=True)
     assert flags & optcc.OCC_F_RANK_DEFICIENT
     assert not (flags & optcc.OCC_F_NONFINITE)
@@ -170,35 +185,40 @@ def test_zero_input_sets_rank_deficient_flag():
     assert optcc.occ_get_flags(ws) == 0
 
 
-def test_exact_low_rank_recovery_and_full_rank():
+@pytest.mark.parametrize("rank,full", [(8, 40), (48, 100)])
+def test_exact_low_rank_recovery_and_full_rank(rank, full):
     from paper_2301_09830_amd import optcc
     torch = torch_mod()
     g = np.random.default_rng(3)
     A = (g.standard_normal((300, 3)) @ g.standard_normal((3, 120))).astype(np.float32)
     M = torch.from_numpy(A).cuda()
     err = torch.zeros_like(M)
-    Q = torch.from_numpy(g.standard_normal((120, 8)).astype(np.float32)).cuda()
-    P, Mh = optcc.occ_step(M, err, Q, 8, 1)
+    Q = torch.from_numpy(g.standard_normal((120, rank)).astype(np.float32)).cuda()
+    P, Mh = optcc.occ_step(M, err, Q, rank, 1)
     torch.cuda.synchronize()
     assert err.norm().item() <= 1e-5 * M.norm().item()
-    # rank = min(m, n): reconstruction equals the input
-    B = torch.from_numpy(g.standard_normal((90, 40)).astype(np.float32)).cuda()
+    # rank = min(m, n): reconstruction equals the input.  An orthonormal
+    # warm start keeps cond(P) <= cond(B)^3 (about 50 for a 3:1 Gaussian),
+    # so the fp32 subspace error stays far below the bound.
+    B = torch.from_numpy(g.standard_normal((3 * full, full)).astype(np.float32)).cuda()
     errb = torch.zeros_like(B)
-    Qb = torch.from_numpy(g.standard_normal((40, 40)).astype(np.float32)).cuda()
-    P, Mh = optcc.occ_step(B, errb, Qb, 40, 2)
+    q_orth, _ = np.linalg.qr(g.standard_normal((full, full)))
+    Qb = torch.from_numpy(q_orth.astype(np.float32)).cuda()
+    P, Mh = optcc.occ_step(B, errb, Qb, full, 2)
     torch.cuda.synchronize()
     assert (Mh - B).norm().item() <= 1e-4 * B.norm().item()
 
 
-def test_nonfinite_input_propagates_and_flags():
+@pytest.mark.parametrize("rank", [4, 96])
+def test_nonfinite_input_propagates_and_flags(rank):
     from paper_2301_09830_amd import optcc
     torch = torch_mod()
     M = torch.randn((256, 128), device="cuda")
     M[17, 5] = float("nan")
     err = torch.zeros_like(M)
-    Q = torch.randn((128, 4), device="cuda")
-    ws = optcc.alloc_workspace(optcc.occ_workspace_bytes([(256, 128)], 4, 1))
-    P, Mh = optcc.occ_step(M, err, Q, 4, 1, ws=ws)
+    Q = torch.randn((128, rank), device="cuda")
+    ws = optcc.alloc_workspace(optcc.occ_workspace_bytes([(256, 128)], rank, 1))
+    P, Mh = optcc.occ_step(M, err, Q, rank, 1, ws=ws)
     flags = optcc.occ_get_flags(ws)
     assert flags & optcc.OCC_F_NONFINITE
     assert torch.isnan(Mh).any() and torch.isnan(err).any()
