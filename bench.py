@@ -34,6 +34,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "compress+decompress+err-update input GB/s and % of HBM roofline, 1 MI355X"
 HBM_PEAK_GBS = 8000.0
+FP32_MFMA_PEAK_TFLOPS = 157.3     # dense fp32 matrix-core peak of the MI355X
 PROFILES = os.path.join(ROOT, "profiles")
 CSRC = os.path.join(ROOT, "paper_2301_09830_amd", "csrc")
 
@@ -54,18 +55,33 @@ def kernel_source_digest() -> str:
 def kernel_alg_bytes(kernel: str, elements: int, m_bytes: int) -> int | None:
     """Bytes one launch of a streaming kernel must move for `elements` of M.
 
-    pass_p / pass_q read M and err once (m_bytes + 4 per element);
-    mhat_err reads M and err and writes err and M_hat (m_bytes + 12);
-    err_only reads M and err and writes err (m_bytes + 8).
+    Passes named without a suffix read M and err_prev (m_bytes + 4 per
+    element); pass_p_first also stores A = M + err_prev over err (+4); the
+    passes named *_a read that stored A back (4).  The reconstruction pass
+    writes err (+4) and M_hat (+4) on top of its reads.
     """
     per = {"pass_p": m_bytes + 4, "pass_q": m_bytes + 4, "mhat_err": m_bytes + 12,
-           "err_only": m_bytes + 8}.get(kernel)
+           "err_only": m_bytes + 8, "pass_p_first": m_bytes + 8, "pass_p_a": 4,
+           "pass_q_a": 4, "mhat_err_a": 12, "err_only_a": 8}.get(kernel)
     return None if per is None else per * elements
 
 
+def kernel_alg_flops(kernel: str, elements: int, rank: int) -> int | None:
+    """Flops of one launch of a product kernel: 2 r per element of M (the
+    left and right products and the reconstruction each do r FMAs)."""
+    if kernel.split("_")[0] in ("pass", "mhat") or kernel.startswith("err_only"):
+        return 2 * rank * elements
+    return None
+
+
 def step_alg_bytes(elements: int, m_bytes: int, iters: int, write_mhat: bool = True) -> int:
-    """2*iters+1 streaming passes over M and err, plus the err (and M_hat) writes."""
-    return elements * ((2 * iters + 1) * (m_bytes + 4) + 4 + (4 if write_mhat else 0))
+    """Algorithmic bytes of one step: the cheaper of re-reading M and err in
+    each of the 2t+1 passes (X) and storing A in the first pass to read it
+    back afterwards (Y), plus the err and M_hat writes."""
+    out = 4 + (4 if write_mhat else 0)
+    x = (2 * iters + 1) * (m_bytes + 4) + out
+    y = (m_bytes + 8) + 4 * (2 * iters - 1) + 4 + out
+    return elements * min(x, y)
 
 
 def load_traffic(kernel: str, workload: str, launches_elements: int):
@@ -144,15 +160,30 @@ def cpu_baseline(w, host, seconds: float):
 # ----------------------------------------------------------------------------
 # rocprofv3 summaries -> profiles/ (host-side text processing, no GPU)
 # ----------------------------------------------------------------------------
-PROFILE_KERNELS = {  # library kernel -> name used in per-kernel timings
-    "k_mh16": "mhat_err", "k_pm": "pass_p", "k_qm": "pass_q", "k_orth16": "orth",
-    "k_qred16": "q_reduce",
-}
-
-
-def _short(kname: str) -> str:
-    base = kname.split("(")[0].replace("void ", "").replace("occ::", "")
-    return base.split("<")[0]
+def profile_name(kname: str) -> str | None:
+    """Launch name (as in the per-kernel timings) of a library kernel, from its
+    demangled name as rocprofv3 reports it."""
+    base = kname.split("(")[0].replace("void ", "").replace("occ::", "").strip()
+    short = base.split("<")[0]
+    args = [a.strip() for a in base[len(short) + 1:-1].split(",")] if "<" in base else []
+    fixed = {"k_pm": "pass_p", "k_qm": "pass_q", "k_orth16": "orth", "k_qred16": "q_reduce",
+             "k_qred": "q_reduce", "k_qpad": "qpad"}
+    if short in fixed:
+        return fixed[short]
+    if short == "k_mh16":
+        return "mhat_err" if args[-1] == "true" else "err_only"
+    if short == "k_lp":
+        return {"0": "pass_p", "1": "pass_p_first", "2": "pass_p_a"}[args[2]]
+    if short == "k_lq":
+        return {"0": "pass_q", "2": "pass_q_a"}[args[2]]
+    if short == "k_ml":
+        if args[3] == "1":
+            return "decompress"
+        return "mhat_err_a" if args[4] == "true" else "err_only_a"
+    pair = {"k_lg": "gram", "k_gsum": "gram_sum", "k_lchol": "chol", "k_lapply": "apply"}
+    if short in pair:
+        return pair[short] + ("2" if args[-1] == "1" else "")
+    return None
 
 
 def write_profiles(workload: str, trace_dir: str, fetch_dir: str, write_dir: str,
@@ -182,8 +213,7 @@ def write_profiles(workload: str, trace_dir: str, fetch_dir: str, write_dir: str
         cal_write = calib_bytes / (write[k] * 1024.0)
     digest = kernel_source_digest()
     for r in rows:
-        short = _short(r["Name"])
-        name = PROFILE_KERNELS.get(short)
+        name = profile_name(r["Name"])
         if name is None:
             continue
         fk = next((k for k in fetch if k.split("(")[0] == r["Name"].split("(")[0]), None)
@@ -329,12 +359,21 @@ def main() -> int:
             launches, total_ms = prof[dom]
             avg_s = total_ms / launches * 1e-3
             per_launch = kernel_alg_bytes(dom, elements, m_bytes)  # one launch covers the batch
-            achieved = per_launch / avg_s / 1e9
+            flops = kernel_alg_flops(dom, elements, w.rank)
             traffic = load_traffic(dom, w.name, elements)
-            roofline = {"kernel": dom, "bound": "hbm", "achieved": round(achieved, 1),
-                        "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                        "frac": round(achieved / HBM_PEAK_GBS, 4),
+            # the bound is whichever resource the kernel's algorithmic work
+            # needs longer on: HBM bytes at 8 TB/s or fp32 MFMA flops
+            mfma_bound = flops is not None and flops / FP32_MFMA_PEAK_TFLOPS > per_launch / HBM_PEAK_GBS * 1e3
+            if mfma_bound:
+                achieved, peak, unit = flops / avg_s / 1e12, FP32_MFMA_PEAK_TFLOPS, "TFLOP/s"
+            else:
+                achieved, peak, unit = per_launch / avg_s / 1e9, HBM_PEAK_GBS, "GB/s"
+            roofline = {"kernel": dom, "bound": "mfma" if mfma_bound else "hbm",
+                        "achieved": round(achieved, 1), "peak": peak, "unit": unit,
+                        "frac": round(achieved / peak, 4),
                         "traffic": traffic, "alg_bytes_per_launch": int(per_launch),
+                        "alg_flops_per_launch": flops,
+                        "hbm_achieved_gbs": round(per_launch / avg_s / 1e9, 1),
                         "avg_launch_us": round(avg_s * 1e6, 3)}
 
     if args.calibrate_copy_mib:

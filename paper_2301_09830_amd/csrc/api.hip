@@ -351,7 +351,7 @@ occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, h
           else if (it == 0)
             L("pass_p_first", k_lp<DT, RP, SA_MERR_SAVE>, b.blocks[K_PASS_P]);
           else
-            L("pass_p", k_lp<DT_F32, RP, SA_SAVED>, b.blocks[K_PASS_P]);
+            L("pass_p_a", k_lp<DT_F32, RP, SA_SAVED>, b.blocks[K_PASS_P]);
           L("gram", k_lg<RP, 0>, b.blocks[K_PGRAM]);
           L("gram_sum", k_gsum<RP, 0>, b.blocks[K_GSUM]);
           LB("chol", k_lchol<RP, 0>, count, LC_THREADS, flags);
@@ -361,16 +361,16 @@ occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, h
           LB("chol2", k_lchol<RP, 1>, count, LC_THREADS, flags);
           L("apply2", k_lapply<RP, 1>, b.blocks[K_APPLY]);
           if (saved)
-            L("pass_q", k_lq<DT_F32, RP, SA_SAVED>, b.blocks[K_PASS_Q]);
+            L("pass_q_a", k_lq<DT_F32, RP, SA_SAVED>, b.blocks[K_PASS_Q]);
           else
             L("pass_q", k_lq<DT, RP, SA_MERR>, b.blocks[K_PASS_Q]);
           L("q_reduce", k_qred<RP>, b.blocks[K_QRED]);
         }
         if (finish) {
           if (write_mhat)
-            L("mhat_err", k_ml<DT_F32, RP, SA_SAVED, 0, true, true>, b.blocks[K_MHAT]);
+            L("mhat_err_a", k_ml<DT_F32, RP, SA_SAVED, 0, true, true>, b.blocks[K_MHAT]);
           else
-            L("err_only", k_ml<DT_F32, RP, SA_SAVED, 0, false, true>, b.blocks[K_MHAT]);
+            L("err_only_a", k_ml<DT_F32, RP, SA_SAVED, 0, false, true>, b.blocks[K_MHAT]);
         }
       }
     });

@@ -58,12 +58,31 @@ class GpuState:
         self.M_hat = self.Mh_full[:, :n]
 
 
+def check_invariants(M_dev, err_prev, err, P, M_hat, label: str):
+    """Properties every step satisfies at any size, checked on the GPU:
+    M_hat + err == M + err_prev up to one fp32 rounding of err, P_hat has
+    orthonormal columns, and the residual is orthogonal to span(P_hat)."""
+    torch = torch_mod()
+    A = M_dev.float() + err_prev
+    amax = A.abs().max().item()
+    cons = (M_hat.double() + err.double() - A.double()).abs().max().item()
+    assert cons <= 2 * np.finfo(np.float32).eps * amax, f"{label}: M_hat + err != A ({cons:.3e})"
+    Pd = P.double()
+    r = P.shape[1]
+    orth = (Pd.T @ Pd - torch.eye(r, dtype=torch.float64, device=P.device)).abs().max().item()
+    assert orth <= 1e-5, f"{label}: P_hat^T P_hat - I = {orth:.3e}"
+    res = (Pd.T @ err.double()).abs().max().item()
+    assert res <= 1e-4 * err.double().norm().item(), f"{label}: P_hat^T err = {res:.3e}"
+
+
 def run_workload(w, steps: int, batched: bool | None = None, ld_pad: int = 0,
-                 check_oracle: bool = True, oracle_mats=None, on_step=None):
+                 check_oracle: bool = True, oracle_mats=None, on_step=None,
+                 invariants_all: bool = False):
     """Run `steps` steps of workload w on the GPU and (optionally) the oracle.
 
     Returns a list of per-step lists of per-matrix dicts with rel_F errors.
     oracle_mats: indices of the matrices the oracle follows (default: all).
+    invariants_all: also check check_invariants() on every matrix.
     """
     from paper_2301_09830_amd import optcc
     torch = torch_mod()
@@ -89,6 +108,7 @@ def run_workload(w, steps: int, batched: bool | None = None, ld_pad: int = 0,
                 dev_M.append(to_device(full, w.m_dtype)[:, :x.shape[1]])
         else:
             dev_M = [to_device(x, w.m_dtype) for x in host_M]
+        prev = [st.err.clone() for st in states] if invariants_all else None
         if batched:
             items = [(dev_M[j], st.err, st.Q, st.P, st.M_hat) for j, st in enumerate(states)]
             optcc.occ_step_batched(items, w.rank, w.iters, ws=ws)
@@ -97,6 +117,11 @@ def run_workload(w, steps: int, batched: bool | None = None, ld_pad: int = 0,
                 optcc.occ_step(dev_M[j], st.err, st.Q, w.rank, w.iters, P=st.P,
                                M_hat=st.M_hat, ws=ws)
         torch.cuda.synchronize()
+        if invariants_all:
+            for j, st in enumerate(states):
+                check_invariants(dev_M[j], prev[j], st.err, st.P, st.M_hat,
+                                 f"{w.name} step {s} matrix {j}")
+            del prev
         step_res = []
         for j in follow:
             st = states[j]
