@@ -327,7 +327,7 @@ occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, h
           for (int it = 0; it < b.iters; ++it) {
             LB("pass_p", k_pm<DT, VEC, RP>, b.blocks[K_PASS_P], PM_THREADS);
             LB("orth", k_orth16<RP>, b.blocks[K_PGRAM], CH_THREADS, flags);
-            L("pass_q", k_qm<DT, VEC, RP>, b.blocks[K_PASS_Q]);
+            LB("pass_q", k_qm<DT, VEC, RP>, b.blocks[K_PASS_Q], QM_THREADS);
             L("q_reduce", k_qred16<RP>, b.blocks[K_QRED]);
           }
           if (finish) {

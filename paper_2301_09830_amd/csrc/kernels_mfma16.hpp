@@ -37,6 +37,8 @@ constexpr int PM_WAVES = 8;               // waves per block in k_pm
 constexpr int PM_THREADS = PM_WAVES * kWave;
 static_assert(PM_ROWS == F_PROWS, "k_pm block rows must match the plan");
 constexpr int QM_COLS = F_QCOLS;          // columns per block in k_qm
+constexpr int QM_WAVES = 8;               // waves per block in k_qm (each a contiguous share of the split's rows)
+constexpr int QM_THREADS = QM_WAVES * kWave;
 
 __device__ __forceinline__ f4v mfma4(float a, float b, f4v c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
@@ -212,14 +214,14 @@ __global__ __launch_bounds__(PM_THREADS) void k_pm(OCC_KARGS) {
 
 // -------------------------------------------------------------------------
 // k_qm: right product partials on MFMA.  A block owns 128 columns and a row
-// split; each wave takes a contiguous quarter of the split's rows in 4-row
-// K-steps.  The B operand is P_hat[row][li], read from the P_hat buffer.
-// The four waves' partial tiles are summed in LDS in wave order and stored
-// to qpart[split].
+// split; each of its QM_WAVES waves takes a contiguous share of the split's
+// rows in 4-row K-steps.  The B operand is P_hat[row][li], read from the
+// P_hat buffer.  The waves' partial tiles are summed in LDS in wave order and
+// stored to qpart[split].
 // -------------------------------------------------------------------------
 struct QMSmem {
   union {
-    float red[4 * QM_COLS * 16];    // per-wave partial tiles
+    float red[QM_WAVES * QM_COLS * 16];    // per-wave partial tiles
   } u;
 };
 
@@ -236,7 +238,7 @@ __device__ __forceinline__ void qm_body(const Desc& d, int b, QMSmem& sm) {
 
   const float* ps = p_src<RP>(d);
 
-  const int wr = (nr + 3) / 4;
+  const int wr = (nr + QM_WAVES - 1) / QM_WAVES;
   const int w_lo = r_lo + min(nr, wave * wr), w_hi = r_lo + min(nr, wave * wr + wr);
   const int nk = (w_hi - w_lo + 3) / 4;
   const int col = c0 + 8 * li;
@@ -276,20 +278,19 @@ __device__ __forceinline__ void qm_body(const Desc& d, int b, QMSmem& sm) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) red[(8 * (4 * g + v) + t) * 16 + li] = acc[t][v];
   __syncthreads();
-  for (int e = threadIdx.x; e < QM_COLS * RP; e += kBlock) {
+  for (int e = threadIdx.x; e < QM_COLS * RP; e += QM_THREADS) {
     const int cl = e / RP, k = e % RP;
     const int gcol = c0 + cl;
     if (gcol >= d.n) continue;
     float v = sm.u.red[cl * 16 + k];
-    v = v + sm.u.red[QM_COLS * 16 + cl * 16 + k];
-    v = v + sm.u.red[2 * QM_COLS * 16 + cl * 16 + k];
-    v = v + sm.u.red[3 * QM_COLS * 16 + cl * 16 + k];
+#pragma unroll
+    for (int w = 1; w < QM_WAVES; ++w) v = v + sm.u.red[w * QM_COLS * 16 + cl * 16 + k];
     d.qpart[((int64_t)s * d.n + gcol) * RP + k] = v;
   }
 }
 
 template <int DT, bool VEC, int RP>
-__global__ __launch_bounds__(kBlock) void k_qm(OCC_KARGS) {
+__global__ __launch_bounds__(QM_THREADS) void k_qm(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) QMSmem sm;
 #define B_(d, b) qm_body<DT, VEC, RP>(d, b, sm)
   OCC_DISPATCH(K_PASS_Q, B_)
