@@ -183,6 +183,14 @@ __device__ __forceinline__ void a_store(const Desc& d, bool vec, int row, int c,
   }
 }
 
+// First column of K-step `it` of a split starting at c_lo whose walk starts at
+// K-step ks0 and wraps around after nk steps (it < nk).
+__device__ __forceinline__ int kcol_of(int c_lo, int ks0, int it, int nk) {
+  int k = ks0 + it;
+  if (k >= nk) k -= nk;
+  return c_lo + L_KC * k;
+}
+
 // -------------------------------------------------------------------------
 // k_lp: P partials = A Q for one 128-row tile and one column split.
 // -------------------------------------------------------------------------
@@ -215,35 +223,48 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b, LPSmem<RP>& sm) {
   for (int u = 0; u < NU; ++u) acc[u] = f16v{};
 
   // qpad has n_pad (a multiple of 32) rows, so every K-step's Q tile is in
-  // bounds; its rows past n are zero.
-  f4v qr[QF4];
-  int kc = c_lo + L_KC * ks0;
+  // bounds; its rows past n are zero.  Q tiles are fetched LP_QAHEAD K-steps
+  // before they are needed (a register ring) and written to the LDS buffer
+  // of the next K-step at the end of each step; A loads run LP_DEPTH K-steps
+  // ahead.
+  constexpr int LP_QAHEAD = RP >= 128 ? 1 : 3;
+  constexpr int LP_DEPTH = RP >= 128 ? 2 : 1;
+  f4v qr[LP_QAHEAD][QF4];
 #pragma unroll
-  for (int x = 0; x < QF4; ++x)
-    qr[x] = *(const f4v*)(d.qpad + (int64_t)kc * RP + 4 * (threadIdx.x + kBlock * x));
+  for (int y = 0; y < LP_QAHEAD; ++y)
+    if (y < nk) {
+      const int c = kcol_of(c_lo, ks0, y, nk);
+#pragma unroll
+      for (int x = 0; x < QF4; ++x)
+        qr[y][x] = *(const f4v*)(d.qpad + (int64_t)c * RP + 4 * (threadIdx.x + kBlock * x));
+    }
 #pragma unroll
   for (int x = 0; x < QF4; ++x) {
     const int f = 4 * (threadIdx.x + kBlock * x);
-    *(f4v*)(&sm.q[0][(f / RP) * QP + f % RP]) = qr[x];
+    *(f4v*)(&sm.q[0][(f / RP) * QP + f % RP]) = qr[0][x];
   }
-  RawA<DT, SA, 16> cur = rawa_load<DT, SA, 16>(d, vec, row, kc + 16 * g, c_hi), nxt;
+  RawA<DT, SA, 16> ring[LP_DEPTH + 1];
+#pragma unroll
+  for (int x = 0; x <= LP_DEPTH; ++x)
+    if (x < nk) ring[x] = rawa_load<DT, SA, 16>(d, vec, row, kcol_of(c_lo, ks0, x, nk) + 16 * g, c_hi);
   __syncthreads();
 
+  int kc = kcol_of(c_lo, ks0, 0, nk);
   for (int it = 0; it < nk; ++it) {
-    const bool more = it + 1 < nk;
-    int kn = 0;
-    if (more) {
-      int k = ks0 + it + 1;
-      if (k >= nk) k -= nk;
-      kn = c_lo + L_KC * k;
+    // Q ring: slot y holds K-step it + y; fetch K-step it + LP_QAHEAD
+#pragma unroll
+    for (int y = 0; y + 1 < LP_QAHEAD; ++y)
+#pragma unroll
+      for (int x = 0; x < QF4; ++x) qr[y][x] = qr[y + 1][x];
+    if (it + LP_QAHEAD < nk) {
+      const int c = kcol_of(c_lo, ks0, it + LP_QAHEAD, nk);
 #pragma unroll
       for (int x = 0; x < QF4; ++x)
-        qr[x] = *(const f4v*)(d.qpad + (int64_t)kn * RP + 4 * (threadIdx.x + kBlock * x));
-      nxt = rawa_load<DT, SA, 16>(d, vec, row, kn + 16 * g, c_hi);
+        qr[LP_QAHEAD - 1][x] = *(const f4v*)(d.qpad + (int64_t)c * RP + 4 * (threadIdx.x + kBlock * x));
     }
     float a[16];
 #pragma unroll
-    for (int j = 0; j < 16; ++j) a[j] = rawa_val<DT, SA, 16>(cur, j);
+    for (int j = 0; j < 16; ++j) a[j] = rawa_val<DT, SA, 16>(ring[0], j);
     if constexpr (SA == SA_MERR_SAVE) a_store<16>(d, vec, row, kc + 16 * g, c_hi, a);
     const float* qb = sm.q[it & 1] + 16 * g * QP + NU * li;
 #pragma unroll
@@ -253,14 +274,18 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b, LPSmem<RP>& sm) {
 #pragma unroll
       for (int u = 0; u < NU; ++u) acc[u] = mfma32(a[j], bv[u], acc[u]);
     }
-    if (more) {
+#pragma unroll
+    for (int x = 0; x < LP_DEPTH; ++x) ring[x] = ring[x + 1];
+    if (it + LP_DEPTH + 1 < nk)
+      ring[LP_DEPTH] = rawa_load<DT, SA, 16>(d, vec, row, kcol_of(c_lo, ks0, it + LP_DEPTH + 1, nk) + 16 * g, c_hi);
+    if (it + 1 < nk) {
+      // slot 0 now holds K-step it + 1
 #pragma unroll
       for (int x = 0; x < QF4; ++x) {
         const int f = 4 * (threadIdx.x + kBlock * x);
-        *(f4v*)(&sm.q[(it + 1) & 1][(f / RP) * QP + f % RP]) = qr[x];
+        *(f4v*)(&sm.q[(it + 1) & 1][(f / RP) * QP + f % RP]) = qr[0][x];
       }
-      cur = nxt;
-      kc = kn;
+      kc = kcol_of(c_lo, ks0, it + 1, nk);
     }
     __syncthreads();
   }
@@ -641,12 +666,18 @@ __device__ __forceinline__ void lq_body(const Desc& d, int b, LQSmem<RP>& sm) {
 #pragma unroll
     for (int u = 0; u < NU; ++u) acc[x][u] = f16v{};
 
-  f4v pr = f4v{0.f, 0.f, 0.f, 0.f};
-  if (t < PF) {
-    const int row = r_lo + pi;
-    if (row < r_hi) pr = *(const f4v*)(d.phat + (int64_t)row * RP + pk);
-    *(f4v*)(&sm.p[0][pi][pk]) = pr;
+  // P_hat rows of a group are fetched LQ_PAHEAD groups before they are
+  // needed (a register ring) and written to the LDS buffer of the next group
+  // at the end of each group; A loads run one group ahead.
+  constexpr int LQ_PAHEAD = 3;
+  f4v pr[LQ_PAHEAD];
+#pragma unroll
+  for (int y = 0; y < LQ_PAHEAD; ++y) {
+    pr[y] = f4v{0.f, 0.f, 0.f, 0.f};
+    const int row = r_lo + L_QG * y + pi;
+    if (t < PF && row < r_hi) pr[y] = *(const f4v*)(d.phat + (int64_t)row * RP + pk);
   }
+  if (t < PF) *(f4v*)(&sm.p[0][pi][pk]) = pr[0];
   RawA<DT, SA, CPL> cur[4], nxt[4];
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
@@ -658,11 +689,14 @@ __device__ __forceinline__ void lq_body(const Desc& d, int b, LQSmem<RP>& sm) {
   for (int grp = 0; grp < ngrp; ++grp) {
     const bool more = grp + 1 < ngrp;
     const int rn = r_lo + L_QG * (grp + 1);
+#pragma unroll
+    for (int y = 0; y + 1 < LQ_PAHEAD; ++y) pr[y] = pr[y + 1];
+    {
+      const int row = r_lo + L_QG * (grp + LQ_PAHEAD) + pi;
+      pr[LQ_PAHEAD - 1] = f4v{0.f, 0.f, 0.f, 0.f};
+      if (t < PF && row < r_hi) pr[LQ_PAHEAD - 1] = *(const f4v*)(d.phat + (int64_t)row * RP + pk);
+    }
     if (more) {
-      if (t < PF) {
-        const int row = rn + pi;
-        pr = row < r_hi ? *(const f4v*)(d.phat + (int64_t)row * RP + pk) : f4v{0.f, 0.f, 0.f, 0.f};
-      }
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         const int row = rn + 2 * ks + g;
@@ -681,7 +715,8 @@ __device__ __forceinline__ void lq_body(const Desc& d, int b, LQSmem<RP>& sm) {
       }
     }
     if (more) {
-      if (t < PF) *(f4v*)(&sm.p[(grp + 1) & 1][pi][pk]) = pr;
+      // slot 0 now holds group grp + 1
+      if (t < PF) *(f4v*)(&sm.p[(grp + 1) & 1][pi][pk]) = pr[0];
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) cur[ks] = nxt[ks];
     }
