@@ -171,7 +171,9 @@ def profile_name(kname: str) -> str | None:
     if short in fixed:
         return fixed[short]
     if short == "k_mh16":
-        return "mhat_err" if args[-1] == "true" else "err_only"
+        if args[3] == "1":
+            return "decompress"
+        return "mhat_err" if args[4] == "true" else "err_only"
     if short == "k_lp":
         return {"0": "pass_p", "1": "pass_p_first", "2": "pass_p_a"}[args[2]]
     if short == "k_lq":

@@ -332,9 +332,9 @@ occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, h
           }
           if (finish) {
             if (write_mhat)
-              L("mhat_err", k_mh16<DT, VEC, RP, true>, b.blocks[K_MHAT]);
+              L("mhat_err", k_mh16<DT, VEC, RP, 0, true, true>, b.blocks[K_MHAT]);
             else
-              L("err_only", k_mh16<DT, VEC, RP, false>, b.blocks[K_MHAT]);
+              L("err_only", k_mh16<DT, VEC, RP, 0, false, true>, b.blocks[K_MHAT]);
           }
           return;
         }
@@ -519,12 +519,13 @@ occ_status_t occ_decompress(const float* P, const float* Q, int64_t m, int64_t n
                            dim3(grid_of(t.blocks[K_MHAT])), dim3(kBlock), 0, s,
                            (const Desc*)nullptr, 1, d);
       } else if (vec) {
-        hipLaunchKernelGGL((k_mhat<DT_F32, true, RP, 1, true, false>),
-                           dim3(grid_of(mhat_blocks(m, n, RP))), dim3(kBlock), 0, s,
+        // same code as the fused step's reconstruction pass
+        hipLaunchKernelGGL((k_mh16<DT_F32, true, RP, 1, true, false>),
+                           dim3(grid_of(t.blocks[K_MHAT])), dim3(kBlock), 0, s,
                            (const Desc*)nullptr, 1, d);
       } else {
-        hipLaunchKernelGGL((k_mhat<DT_F32, false, RP, 1, true, false>),
-                           dim3(grid_of(mhat_blocks(m, n, RP))), dim3(kBlock), 0, s,
+        hipLaunchKernelGGL((k_mh16<DT_F32, false, RP, 1, true, false>),
+                           dim3(grid_of(t.blocks[K_MHAT])), dim3(kBlock), 0, s,
                            (const Desc*)nullptr, 1, d);
       }
     });

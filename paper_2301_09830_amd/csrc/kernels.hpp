@@ -172,93 +172,6 @@ __global__ __launch_bounds__(kBlock) void k_qred(OCC_KARGS) {
 }
 
 // ---------------------------------------------------------------------------
-// Reconstruction and residual in one pass:
-//   M_hat[i,c] = sum_k P_hat[i,k] Q[c,k]  (k ascending, fmaf from 0)
-//   err[i,c]   = (M[i,c] + err_prev[i,c]) - M_hat[i,c]
-// Each lane owns CPL columns and keeps their Q rows in VGPRs; rows of P_hat
-// come from SGPRs.  SRC selects where the factors come from:
-//   0: the workspace's padded phat/qpad (fused step)
-//   1: the caller's P (m x r) and Q (n x r) (stand-alone decompression)
-// ---------------------------------------------------------------------------
-template <int DT, bool VEC, int RP, int SRC, bool WRITE_MHAT, bool WRITE_ERR>
-__device__ __forceinline__ void mhat_body(const Desc& d, int b) {
-  constexpr int CPL = cols_per_lane(RP);
-  const int wave = wave_id(), lane = threadIdx.x & 63;
-  const int col_tiles = (d.n + 64 * CPL - 1) / (64 * CPL);
-  const int ct = b % col_tiles, rb = b / col_tiles;
-  const int c0 = ct * 64 * CPL + lane * CPL;
-  const int r_lo = rb * MH_ROWS;
-  const int r_hi = min(d.m, r_lo + MH_ROWS);
-
-  float q[CPL][RP];
-#pragma unroll
-  for (int j = 0; j < CPL; ++j) {
-    const int c = c0 + j;
-#pragma unroll
-    for (int k = 0; k < RP; ++k) {
-      float v = 0.f;
-      if (c < d.n) {
-        if (SRC == 0) v = d.qpad[(int64_t)c * RP + k];
-        else if (k < d.r) v = d.Q[(int64_t)c * d.r + k];
-      }
-      q[j][k] = v;
-    }
-  }
-
-  for (int i = r_lo + wave; i < r_hi; i += 4) {
-    float ph[RP];
-    if (SRC == 0) {
-      const cfloat_p p = as_const(d.phat) + (int64_t)i * RP;
-#pragma unroll
-      for (int k = 0; k < RP; ++k) ph[k] = p[k];
-    } else {
-      const cfloat_p p = as_const(d.P) + (int64_t)i * d.r;
-#pragma unroll
-      for (int k = 0; k < RP; ++k) ph[k] = (k < d.r) ? p[k] : 0.f;
-    }
-    float mh[CPL];
-#pragma unroll
-    for (int j = 0; j < CPL; ++j) {
-      float s = 0.f;
-#pragma unroll
-      for (int k = 0; k < RP; ++k) s = fmaf(ph[k], q[j][k], s);
-      mh[j] = s;
-    }
-    if (WRITE_MHAT) {
-      const int64_t ho = (int64_t)i * d.ldh + c0;
-      if (CPL == 4 && VEC && c0 + 4 <= d.n) {
-        *(float4*)(d.Mhat + ho) = make_float4(mh[0], mh[1 % CPL], mh[2 % CPL], mh[3 % CPL]);
-      } else {
-#pragma unroll
-        for (int j = 0; j < CPL; ++j) if (c0 + j < d.n) d.Mhat[ho + j] = mh[j];
-      }
-    }
-    if (WRITE_ERR) {
-      float a[CPL];
-      if (CPL == 4) load_a4<DT, VEC>(d, i, c0, d.n, a);
-      else a[0] = load_a1<DT>(d, i, c0);
-      float e[CPL];
-#pragma unroll
-      for (int j = 0; j < CPL; ++j) e[j] = a[j] - mh[j];
-      const int64_t eo = (int64_t)i * d.lde_out + c0;
-      if (CPL == 4 && VEC && c0 + 4 <= d.n) {
-        *(float4*)(d.err_out + eo) = make_float4(e[0], e[1 % CPL], e[2 % CPL], e[3 % CPL]);
-      } else {
-#pragma unroll
-        for (int j = 0; j < CPL; ++j) if (c0 + j < d.n) d.err_out[eo + j] = e[j];
-      }
-    }
-  }
-}
-
-template <int DT, bool VEC, int RP, int SRC, bool WRITE_MHAT, bool WRITE_ERR>
-__global__ __launch_bounds__(kBlock) void k_mhat(OCC_KARGS) {
-#define B_(d, b) mhat_body<DT, VEC, RP, SRC, WRITE_MHAT, WRITE_ERR>(d, b)
-  OCC_DISPATCH(K_MHAT, B_)
-#undef B_
-}
-
-// ---------------------------------------------------------------------------
 // Stand-alone error update: err_new = (M + err_prev) - M_hat, elementwise,
 // same operation order as the fused pass.
 // ---------------------------------------------------------------------------

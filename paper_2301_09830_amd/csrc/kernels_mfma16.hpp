@@ -23,6 +23,7 @@
 //          (g, li) loads columns 8li..8li+7 of row g and feeds 8 MFMAs, MFMA t
 //          producing the interleaved column tile {8m + t}.  The B operand is
 //          P_hat[row g][li].
+//   k_mh16 M_hat = P_hat Q^T and err = A - M_hat (see below).
 #pragma once
 
 #include "kernels_small.hpp"
@@ -294,6 +295,159 @@ __global__ __launch_bounds__(QM_THREADS) void k_qm(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) QMSmem sm;
 #define B_(d, b) qm_body<DT, VEC, RP>(d, b, sm)
   OCC_DISPATCH(K_PASS_Q, B_)
+#undef B_
+}
+
+// -------------------------------------------------------------------------
+// k_mh16: reconstruction and residual, M_hat = P_hat Q^T and
+// err = A - M_hat.  The products run on v_mfma_f32_16x16x4_f32 in the
+// transposed form M_hat^T = Q P_hat^T: for a 16-row group and a 16-column
+// tile, lane (g, li) supplies Q[col li][k] and P_hat[row li][k] for its
+// K-steps' rank indices k = S g + s (S = RP / 4, MFMA s) and receives
+// M_hat[row li][cols 4g..4g+3].  That layout would write 16 rows x 64 bytes
+// per instruction, so each wave passes its 16 x F_MHCOLS tile through LDS
+// and then reads A, writes M_hat and writes err row-contiguously (32 lanes x
+// 16 bytes per row).  A block is four waves; wave w takes the 16-row groups
+// w, w + 4, ... of the block's d.mr rows, and loads that group's A before
+// its MFMAs so the loads are in flight during them.
+//
+// SRC 0: factors from the step's padded workspace copies (row pitch RP,
+//        read with 16-byte loads).
+// SRC 1: the caller's P (m x r) and Q (n x r) (stand-alone decompression).
+// WRITE_ERR also reads A and writes err; without it only M_hat is written.
+// Both entry points run this same code, so their M_hat agree bitwise.
+// -------------------------------------------------------------------------
+constexpr int MX_LDW = F_MHCOLS + 4;          // LDS row pitch (floats), 16-byte skew per row
+constexpr int MX_LPR = F_MHCOLS / 4;          // lanes per row in the row-contiguous phase
+constexpr int MX_RPI = kWave / MX_LPR;        // rows per instruction in that phase
+constexpr int MX_NCH = 16 / MX_RPI;           // row chunks per lane per 16-row group
+static_assert(F_MHGROUP == 4 * 16, "four waves of 16-row groups per block step");
+
+struct MXSmem {
+  float t[4][16 * MX_LDW];
+};
+
+// Factor values [row][S g .. S g + S - 1] of a lane: from the padded
+// workspace copy (row pitch RP, 256-byte aligned base) with one vector load,
+// or from a caller's m x r array element by element (zero past rank r).
+template <int S>
+__device__ __forceinline__ void factor_vec(const float* p, float v[S]) {
+  if constexpr (S == 4) {
+    const float4 x = *(const float4*)p;
+    v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+  } else if constexpr (S == 2) {
+    const float2 x = *(const float2*)p;
+    v[0] = x.x; v[1] = x.y;
+  } else {
+    v[0] = *p;
+  }
+}
+
+template <int RP, int SRC>
+__device__ __forceinline__ void factor_load(const float* base, int r, int row, bool ok, int k0,
+                                            float v[RP / 4]) {
+  constexpr int S = RP / 4;
+  if (!ok) {
+#pragma unroll
+    for (int s = 0; s < S; ++s) v[s] = 0.f;
+  } else if (SRC == 0) {
+    factor_vec<S>(base + (int64_t)row * RP + k0, v);
+  } else {
+#pragma unroll
+    for (int s = 0; s < S; ++s) v[s] = (k0 + s < r) ? base[(int64_t)row * r + k0 + s] : 0.f;
+  }
+}
+
+template <int DT, bool VEC, int RP, int SRC, bool WRITE_MHAT, bool WRITE_ERR>
+__device__ __forceinline__ void mh16_body(const Desc& d, int b, MXSmem& sm) {
+  constexpr int S = RP / 4;        // MFMA K-steps (rank indices per lane group)
+  constexpr int NTILE = F_MHCOLS / 16;
+  const int wave = wave_id(), lane = threadIdx.x & 63;
+  const int li = lane & 15, g = lane >> 4;
+  const int col_tiles = (d.n + F_MHCOLS - 1) / F_MHCOLS;
+  const int ct = b % col_tiles, rb = b / col_tiles;
+  const int c0 = ct * F_MHCOLS;
+  const int r_lo = rb * d.mr, r_hi = min(d.m, r_lo + d.mr);
+  const float* qs = (SRC == 0) ? d.qpad : d.Q;
+  const float* ps = (SRC == 0) ? d.phat : d.P;
+
+  // A operand of tile t: Q[c0 + 16t + li][S g + s]
+  float qa[NTILE][S];
+#pragma unroll
+  for (int t = 0; t < NTILE; ++t) {
+    const int c = c0 + 16 * t + li;
+    factor_load<RP, SRC>(qs, d.r, c, c < d.n, S * g, qa[t]);
+  }
+  const int cl = 4 * (lane % MX_LPR), rl = lane / MX_LPR;
+  const int col = c0 + cl;
+  const bool vec_col = VEC && col + 4 <= d.n;
+  float* tile = sm.t[wave];
+  for (int r0 = r_lo + 16 * wave; r0 < r_hi; r0 += F_MHGROUP) {
+    AChunk<DT> x[MX_NCH];
+    if (WRITE_ERR) {
+#pragma unroll
+      for (int k = 0; k < MX_NCH; ++k) {
+        const int row = r0 + rl + MX_RPI * k;
+        chunk_issue<DT, VEC>(d, row < r_hi ? row : d.m, col, d.n, x[k]);
+      }
+    }
+    // B operand: P_hat[r0 + li][S g + s]
+    const int rowb = r0 + li;
+    float pb[S];
+    factor_load<RP, SRC>(ps, d.r, rowb, rowb < r_hi, S * g, pb);
+#pragma unroll
+    for (int t = 0; t < NTILE; ++t) {
+      f4v acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < S; ++s) acc = mfma4(qa[t][s], pb[s], acc);
+      *(float4*)(tile + li * MX_LDW + 16 * t + 4 * g) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    }
+    // the tile is written and read by this wave only; LDS keeps a wave's
+    // operations in order, and the wait also orders them for the compiler
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+    for (int k = 0; k < MX_NCH; ++k) {
+      const int rr = rl + MX_RPI * k;
+      const int row = r0 + rr;
+      const float4 mh4 = *(const float4*)(tile + rr * MX_LDW + cl);
+      if (row >= r_hi) continue;
+      const float mh[4] = {mh4.x, mh4.y, mh4.z, mh4.w};
+      float e[4] = {0.f, 0.f, 0.f, 0.f};
+      if (WRITE_ERR) {
+        float a[4];
+        chunk_value<DT>(x[k], a);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) e[j] = a[j] - mh[j];
+      }
+      if (vec_col) {
+        // streaming outputs: nontemporal stores (the dirty lines would
+        // otherwise be written back during the next step's first pass)
+        typedef float nt4 __attribute__((ext_vector_type(4)));
+        if (WRITE_MHAT)
+          __builtin_nontemporal_store(nt4{mh[0], mh[1], mh[2], mh[3]},
+                                      (nt4*)(d.Mhat + (int64_t)row * d.ldh + col));
+        if (WRITE_ERR)
+          __builtin_nontemporal_store(nt4{e[0], e[1], e[2], e[3]},
+                                      (nt4*)(d.err_out + (int64_t)row * d.lde_out + col));
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (col + j < d.n) {
+            if (WRITE_MHAT) d.Mhat[(int64_t)row * d.ldh + col + j] = mh[j];
+            if (WRITE_ERR) d.err_out[(int64_t)row * d.lde_out + col + j] = e[j];
+          }
+        }
+      }
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  }
+}
+
+template <int DT, bool VEC, int RP, int SRC, bool WRITE_MHAT, bool WRITE_ERR>
+__global__ __launch_bounds__(kBlock) void k_mh16(OCC_KARGS) {
+  __shared__ __attribute__((aligned(16))) MXSmem sm;
+#define B_(d, b) mh16_body<DT, VEC, RP, SRC, WRITE_MHAT, WRITE_ERR>(d, b, sm)
+  OCC_DISPATCH(K_MHAT, B_)
 #undef B_
 }
 

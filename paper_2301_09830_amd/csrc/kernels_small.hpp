@@ -17,16 +17,12 @@
 //   k_qred16 Q = sum of the row-split partials.
 // and after the last round
 //   k_mh16   reconstruction and residual, M_hat = P_hat Q^T and
-//            err = A - M_hat (vector ALU: lanes own four columns and keep
-//            their Q rows in VGPRs, rows of P_hat come from SGPRs).
+//            err = A - M_hat (matrix cores, kernels_mfma16.hpp).
 #pragma once
 
 #include "kernels.hpp"
 
 namespace occ {
-
-constexpr int Q16_COLS = F_MHCOLS;        // reconstruction: columns per block (4 per lane)
-constexpr int MH16_ROWS = F_MHROWS;       // rows per block of the reconstruction pass
 
 // -------------------------------------------------------------------------
 // A = M + err_prev in 4-column chunks, split into "issue" and "value" so that
@@ -268,8 +264,8 @@ __device__ __forceinline__ void gram_sum_all(const double* src, int nsrc, CholSm
   __syncthreads();
 }
 
-// P_hat row = P row * T (fp64), written to the caller's P and, when
-// rank < RP, the padded copy.
+// P_hat row = P row * T (fp64), written to the caller's P and the padded
+// copy.
 template <int RP>
 __device__ __forceinline__ void phat_row(const Desc& d, int64_t row, const double* T) {
   // keep the T reads here: hoisting all of them out of a row loop costs ~270 VGPRs
@@ -289,11 +285,11 @@ __device__ __forceinline__ void phat_row(const Desc& d, int64_t row, const doubl
     for (int l = 0; l <= k; ++l) v = fma((double)p[l], T[l * RP + k], v);
     out[k] = (float)v;
   }
-  if (d.r != RP) {
+  // the padded copy is always written: the reconstruction pass reads it with
+  // 16-byte loads (the caller's P has no alignment guarantee)
 #pragma unroll
-    for (int k = 0; k < RP; k += 4)
-      *(float4*)(d.phat + row * RP + k) = make_float4(out[k], out[k + 1], out[k + 2], out[k + 3]);
-  }
+  for (int k = 0; k < RP; k += 4)
+    *(float4*)(d.phat + row * RP + k) = make_float4(out[k], out[k + 1], out[k + 2], out[k + 3]);
 #pragma unroll
   for (int k = 0; k < RP; ++k)
     if (k < d.r) d.P[row * d.r + k] = out[k];
@@ -410,7 +406,7 @@ __global__ __launch_bounds__(CH_THREADS) void k_orth16(OCC_KARGS, uint32_t* flag
 
 // -------------------------------------------------------------------------
 // k_qred16: Q[c][k] = sum over row splits of qpart[s][c][k] (fixed order),
-// written to the caller's Q and, when rank < RP, the padded copy.
+// written to the caller's Q and the padded copy.
 // -------------------------------------------------------------------------
 template <int RP>
 __device__ __forceinline__ void qred16_body(const Desc& d, int b) {
@@ -426,7 +422,7 @@ __device__ __forceinline__ void qred16_body(const Desc& d, int b) {
     for (int u = 0; u < 8; ++u)
       if (t0 + u < d.sq) acc = (t0 + u == 0) ? v[u] : acc + v[u];
   }
-  if (d.r != RP) d.qpad[idx] = acc;
+  d.qpad[idx] = acc;   // always: the reconstruction pass reads the padded copy
   if (k < d.r) d.Q[(int64_t)c * d.r + k] = acc;
 }
 
@@ -434,87 +430,6 @@ template <int RP>
 __global__ __launch_bounds__(kBlock) void k_qred16(OCC_KARGS) {
 #define B_(d, b) qred16_body<RP>(d, b)
   OCC_DISPATCH(K_QRED, B_)
-#undef B_
-}
-
-// -------------------------------------------------------------------------
-// k_mh16: M_hat = P_hat Q^T and err = A - M_hat (same arithmetic as k_mhat).
-// -------------------------------------------------------------------------
-template <int DT, bool VEC, int RP, bool WRITE_MHAT>
-__device__ __forceinline__ void mh16_body(const Desc& d, int b) {
-  const int wave = wave_id(), lane = threadIdx.x & 63;
-  const int col_tiles = (d.n + Q16_COLS - 1) / Q16_COLS;
-  const int ct = b % col_tiles, rb = b / col_tiles;
-  const int c0 = ct * Q16_COLS + lane * 4;
-  const int r_lo = rb * MH16_ROWS;
-  const int r_hi = min(d.m, r_lo + MH16_ROWS);
-  const float* qs = q_src<RP>(d);
-  const float* ps = p_src<RP>(d);
-
-  float q[4][RP];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int c = c0 + j;
-#pragma unroll
-    for (int k = 0; k < RP; ++k) q[j][k] = (c < d.n) ? qs[(int64_t)c * RP + k] : 0.f;
-  }
-  const bool vec_row = VEC && c0 + 4 <= d.n;
-
-  auto finish_row = [&](int row, const AChunk<DT>& x) {
-    const cfloat_p p = as_const(ps) + (int64_t)row * RP;
-    float ph[RP];
-#pragma unroll
-    for (int k = 0; k < RP; ++k) ph[k] = p[k];
-    float mh[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      float s = 0.f;
-#pragma unroll
-      for (int k = 0; k < RP; ++k) s = fmaf(ph[k], q[j][k], s);
-      mh[j] = s;
-    }
-    float a[4];
-    chunk_value<DT>(x, a);
-    const float e0 = a[0] - mh[0], e1 = a[1] - mh[1], e2 = a[2] - mh[2], e3 = a[3] - mh[3];
-    if (vec_row) {
-      // streaming outputs: nontemporal stores (measured +20 % on this pass)
-      typedef float nt4 __attribute__((ext_vector_type(4)));
-      if (WRITE_MHAT)
-        __builtin_nontemporal_store(nt4{mh[0], mh[1], mh[2], mh[3]},
-                                    (nt4*)(d.Mhat + (int64_t)row * d.ldh + c0));
-      __builtin_nontemporal_store(nt4{e0, e1, e2, e3}, (nt4*)(d.err_out + (int64_t)row * d.lde_out + c0));
-    } else {
-      const float ev[4] = {e0, e1, e2, e3};
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if (c0 + j < d.n) {
-          if (WRITE_MHAT) d.Mhat[(int64_t)row * d.ldh + c0 + j] = mh[j];
-          d.err_out[(int64_t)row * d.lde_out + c0 + j] = ev[j];
-        }
-      }
-    }
-  };
-
-  constexpr int U = 4;
-  int i = r_lo + wave;
-  for (; i + (U - 1) * 4 < r_hi; i += U * 4) {
-    AChunk<DT> x[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) chunk_issue<DT, VEC>(d, i + 4 * u, c0, d.n, x[u]);
-#pragma unroll
-    for (int u = 0; u < U; ++u) finish_row(i + 4 * u, x[u]);
-  }
-  for (; i < r_hi; i += 4) {
-    AChunk<DT> x;
-    chunk_issue<DT, VEC>(d, i, c0, d.n, x);
-    finish_row(i, x);
-  }
-}
-
-template <int DT, bool VEC, int RP, bool WRITE_MHAT>
-__global__ __launch_bounds__(kBlock) void k_mh16(OCC_KARGS) {
-#define B_(d, b) mh16_body<DT, VEC, RP, WRITE_MHAT>(d, b)
-  OCC_DISPATCH(K_MHAT, B_)
 #undef B_
 }
 

@@ -30,13 +30,6 @@ enum Kind : int {
   K_NUM
 };
 
-// Tile constants of the stand-alone reconstruction kernel (k_mhat, used by
-// occ_decompress at padded rank <= 16).
-constexpr int MH_ROWS = 64;     // rows per block
-
-// Columns per lane of k_mhat.
-__host__ __device__ constexpr int cols_per_lane(int rp) { return rp <= 16 ? 4 : 1; }
-
 struct Desc {
   // caller buffers
   const void* M;
@@ -67,7 +60,7 @@ struct Desc {
   int32_t blk[K_NUM];    // first block of this matrix in each kernel's grid
   int32_t fused;         // 1: small-rank path (rank padded to <= 16)
   int32_t m_pad;         // large-rank path: rows of phat_t (multiple of 32)
-  int32_t mr;            // large-rank path: rows per block of the reconstruction pass
+  int32_t mr;            // rows per block of the reconstruction pass
   int32_t vec;           // large-rank path: 16-byte vector loads allowed
 };
 
@@ -92,8 +85,9 @@ inline int padded_rank(int r) {
 constexpr int kFusedMaxRank = 16;
 constexpr int F_PROWS = 32;       // left product: rows per block
 constexpr int F_QCOLS = 128;      // right product: columns per block
-constexpr int F_MHROWS = 256;     // reconstruction: rows per block
-constexpr int F_MHCOLS = 256;     // reconstruction: columns per block (4 per lane)
+constexpr int F_MHCOLS = 128;     // reconstruction: columns per block
+constexpr int F_MHGROUP = 64;     // reconstruction: rows per block step (4 waves x 16 rows)
+constexpr int F_MHBLOCKS = 1024;  // reconstruction: target number of blocks
 constexpr int F_QBLOCKS = 512;    // right product: target number of blocks
 constexpr int F_ORTHROWS = 128;   // Cholesky/P_hat kernel: rows of P_hat per block
 
@@ -125,13 +119,17 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp) {
     const int64_t sq = clamp64(cdiv(F_QBLOCKS, col_tiles), 1, cdiv(m, 32));
     t.q_rows = (int)round_up(cdiv(m, sq), 4);
     t.sq = (int)cdiv(m, t.q_rows);
-    t.mr = 0;
+    // reconstruction: 128-column tiles x row blocks (multiple of 64 rows),
+    // about F_MHBLOCKS blocks
+    const int64_t ctm = cdiv(n, F_MHCOLS);
+    const int64_t rbm = clamp64(cdiv(F_MHBLOCKS, ctm), 1, cdiv(m, F_MHGROUP));
+    t.mr = (int)round_up(cdiv(m, rbm), F_MHGROUP);
     t.blocks[K_QPAD] = cdiv((int64_t)t.n_pad * rp, kBlock);
     t.blocks[K_PASS_P] = p_blocks;
     t.blocks[K_PGRAM] = cdiv(m, F_ORTHROWS);
     t.blocks[K_PASS_Q] = col_tiles * t.sq;
     t.blocks[K_QRED] = cdiv(n * rp, kBlock);
-    t.blocks[K_MHAT] = cdiv(n, F_MHCOLS) * cdiv(m, F_MHROWS);
+    t.blocks[K_MHAT] = ctm * cdiv(m, t.mr);
     return t;
   }
   // left product: 128-row tiles; split the columns (>= 1024 per split) until
@@ -162,11 +160,6 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp) {
   t.blocks[K_QRED] = cdiv(n * rp, kBlock);
   t.blocks[K_MHAT] = ctm * cdiv(m, t.mr);
   return t;
-}
-
-// Grid of k_mhat (stand-alone reconstruction at padded rank <= 16).
-inline int64_t mhat_blocks(int64_t m, int64_t n, int rp) {
-  return cdiv(n, (int64_t)kWave * cols_per_lane(rp)) * cdiv(m, MH_ROWS);
 }
 
 // Workspace layout: [header 256 B: sticky flags word][descriptor table]
