@@ -197,11 +197,13 @@ occ_status_t plan_batch(const occ_mat_t* mats, int count, int rank, int iters, u
   b.iters = iters;
   b.fused = b.rp <= kFusedMaxRank;
   size_t off = kHeaderBytes + table_bytes(count);
+  double total_elems = 0.0;
+  for (int j = 0; j < count; ++j) total_elems += (double)mats[j].rows * (double)mats[j].cols;
   b.descs.assign(count, Desc{});
   for (int k = 0; k < K_NUM; ++k) b.blocks[k] = 0;
   for (int j = 0; j < count; ++j) {
     const occ_mat_t& a = mats[j];
-    const Tiling t = make_tiling(a.rows, a.cols, b.rp);
+    const Tiling t = make_tiling(a.rows, a.cols, b.rp, (double)a.rows * (double)a.cols / total_elems);
     const Regions g = matrix_regions(a.rows, a.cols, b.rp, t);
     Desc& d = b.descs[j];
     d.m = (int32_t)a.rows;

@@ -10,6 +10,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 namespace occ {
 
 constexpr int kMaxRank = 128;
@@ -98,6 +100,11 @@ constexpr int L_KC = 32;          // left product: columns per K-step
 constexpr int L_GROWS = 256;      // Gram partials: rows per block
 constexpr int L_AROWS = 128;      // P_hat = P T: rows per block
 constexpr int L_QG = 8;           // right product: rows per LDS stage
+constexpr int64_t L_SPLIT_BLOCKS = 1024;  // split products: blocks over the whole batch
+constexpr int64_t L_MIN_BLOCKS = 256;     // ... and at least this many per matrix
+constexpr int64_t L_MIN_COLS = 1024;      // left product: columns per split, at least
+constexpr int64_t L_MIN_ROWS = 1024;      // right product: rows per split, at least
+constexpr int64_t L_MIN_SPLIT = 512;      // columns / rows per split, at least
 // right product: columns per lane and per block
 __host__ __device__ constexpr int lq_cpl(int rp) { return rp >= 128 ? 1 : 128 / rp; }
 __host__ __device__ constexpr int lq_block_cols(int rp) { return 128 * lq_cpl(rp); }
@@ -105,7 +112,9 @@ __host__ __device__ constexpr int lq_block_cols(int rp) { return 128 * lq_cpl(rp
 __host__ __device__ constexpr int lm_tiles(int rp) { return rp >= 64 ? 1 : 2; }
 __host__ __device__ constexpr int lm_block_cols(int rp) { return 128 * lm_tiles(rp); }
 
-inline Tiling make_tiling(int64_t m, int64_t n, int rp) {
+// share: this matrix's fraction of the elements of the whole call (the
+// large-rank grids are sized for the batch).
+inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0) {
   Tiling t{};
   t.n_pad = (int)round_up(n, 32);
   t.m_pad = (int)round_up(m, 32);
@@ -132,23 +141,28 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp) {
     t.blocks[K_MHAT] = ctm * cdiv(m, t.mr);
     return t;
   }
-  // left product: 128-row tiles; split the columns (>= 1024 per split) until
-  // a matrix has about 256 blocks
+  // Grid sizes.  The split kernels aim at L_SPLIT_BLOCKS blocks over the
+  // whole batch, each matrix taking its share by element count (`share` =
+  // this matrix's fraction of the call's elements), but at least
+  // L_MIN_BLOCKS per matrix; each split adds a partial (rows x rank for the
+  // left product, summed by the Gram kernel; cols x rank for the right
+  // product), so splits stay at least L_MIN_COLS columns / L_MIN_ROWS rows
+  // wide.  The reconstruction has no partials and aims at twice as many.
+  const int64_t target = std::max<int64_t>(L_MIN_BLOCKS, (int64_t)(share * (double)L_SPLIT_BLOCKS + 0.5));
+  // left product: 128-row tiles, columns split
   const int64_t row_tiles = cdiv(m, L_PROWS);
-  const int64_t sp = clamp64(cdiv(256, row_tiles), 1, cdiv(n, 1024));
+  const int64_t sp = clamp64(cdiv(target, row_tiles), 1, cdiv(n, L_MIN_COLS));
   t.p_cols = (int)round_up(cdiv(n, sp), L_KC);
   t.sp = (int)cdiv(n, t.p_cols);
   t.ng = (int)cdiv(m, L_GROWS);
-  // right product: column tiles, rows split (>= 1024 per split) to about
-  // 256 blocks
+  // right product: column tiles, rows split
   const int64_t ctq = cdiv(n, lq_block_cols(rp));
-  const int64_t sq = clamp64(cdiv(256, ctq), 1, cdiv(m, 1024));
+  const int64_t sq = clamp64(cdiv(target, ctq), 1, cdiv(m, L_MIN_ROWS));
   t.q_rows = (int)round_up(cdiv(m, sq), L_QG);
   t.sq = (int)cdiv(m, t.q_rows);
-  // reconstruction: column tiles x row blocks (multiple of 32 rows), about
-  // 512 blocks
+  // reconstruction: column tiles x row blocks (multiple of 32 rows)
   const int64_t ctm = cdiv(n, lm_block_cols(rp));
-  const int64_t rbm = clamp64(cdiv(512, ctm), 1, cdiv(m, 32));
+  const int64_t rbm = clamp64(cdiv(2 * target, ctm), 1, cdiv(m, 32));
   t.mr = (int)round_up(cdiv(m, rbm), 32);
   t.blocks[K_QPAD] = cdiv((int64_t)t.n_pad * rp, kBlock);
   t.blocks[K_PASS_P] = row_tiles * t.sp;
