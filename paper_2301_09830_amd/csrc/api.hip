@@ -169,6 +169,7 @@ void finalize_regions(Batch& b, void* ws) {
     d.tm = (double*)(base + (uintptr_t)d.tm);
     d.info = (uint32_t*)(base + (uintptr_t)d.info);
     d.phat_t = (float*)(base + (uintptr_t)d.phat_t);
+    d.qbf = (uint16_t*)(base + (uintptr_t)d.qbf);
   }
 }
 
@@ -235,6 +236,7 @@ occ_status_t plan_batch(const occ_mat_t* mats, int count, int rank, int iters, u
     d.tm = (double*)(uintptr_t)(off + g.tm);
     d.info = (uint32_t*)(uintptr_t)(off + g.info);
     d.phat_t = (float*)(uintptr_t)(off + g.phat_t);
+    d.qbf = (uint16_t*)(uintptr_t)(off + g.qbf);
     off += g.total;
   }
   b.ws_needed = off;
@@ -270,6 +272,7 @@ occ_status_t plan_batch(const occ_mat_t* mats, int count, int rank, int iters, u
   for (int j = 0; j < count; ++j) {
     const occ_mat_t& a = mats[j];
     Desc& d = b.descs[j];
+    if (dt != OCC_BF16) d.qbf = nullptr;   // the bf16 Q parts serve bf16 M only
     d.M = a.M;
     d.err_in = a.err;
     d.err_out = a.err;
@@ -346,14 +349,16 @@ occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, h
         // first left product stores A over it and every later pass reads A
         // back from there; a compress-only call re-reads M and err_prev.
         const bool saved = b.descs[0].err_out != nullptr;
+        // bf16 M: left products on bf16 matrix cores with split operands
+        constexpr bool X3 = DT == DT_BF16;
         L("qpad", k_qpad<RP>, b.blocks[K_QPAD]);
         for (int it = 0; it < b.iters; ++it) {
           if (!saved)
-            L("pass_p", k_lp<DT, RP, SA_MERR>, b.blocks[K_PASS_P]);
+            L("pass_p", k_lp<DT, RP, SA_MERR, X3>, b.blocks[K_PASS_P]);
           else if (it == 0)
-            L("pass_p_first", k_lp<DT, RP, SA_MERR_SAVE>, b.blocks[K_PASS_P]);
+            L("pass_p_first", k_lp<DT, RP, SA_MERR_SAVE, X3>, b.blocks[K_PASS_P]);
           else
-            L("pass_p_a", k_lp<DT_F32, RP, SA_SAVED>, b.blocks[K_PASS_P]);
+            L("pass_p_a", k_lp<DT_F32, RP, SA_SAVED, X3>, b.blocks[K_PASS_P]);
           L("gram", k_lg<RP, 0>, b.blocks[K_PGRAM]);
           L("gram_sum", k_gsum<RP, 0>, b.blocks[K_GSUM]);
           LB("chol", k_lchol<RP, 0>, count, LC_THREADS, flags);
@@ -362,10 +367,17 @@ occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, h
           L("gram_sum2", k_gsum<RP, 1>, b.blocks[K_GSUM]);
           LB("chol2", k_lchol<RP, 1>, count, LC_THREADS, flags);
           L("apply2", k_lapply<RP, 1>, b.blocks[K_APPLY]);
-          if (saved)
-            L("pass_q_a", k_lq<DT_F32, RP, SA_SAVED>, b.blocks[K_PASS_Q]);
-          else
-            L("pass_q", k_lq<DT, RP, SA_MERR>, b.blocks[K_PASS_Q]);
+          if constexpr (X3) {
+            if (saved)
+              L("pass_q_a", k_lqx<DT_F32, RP, SA_SAVED>, b.blocks[K_PASS_Q]);
+            else
+              L("pass_q", k_lqx<DT, RP, SA_MERR>, b.blocks[K_PASS_Q]);
+          } else {
+            if (saved)
+              L("pass_q_a", k_lq<DT_F32, RP, SA_SAVED>, b.blocks[K_PASS_Q]);
+            else
+              L("pass_q", k_lq<DT, RP, SA_MERR>, b.blocks[K_PASS_Q]);
+          }
           L("q_reduce", k_qred<RP>, b.blocks[K_QRED]);
         }
         if (finish) {
@@ -475,6 +487,7 @@ occ_status_t occ_compress(const void* M, int m_dtype, int64_t m, int64_t n, int6
   if (overlaps(spans)) return OCC_E_ALIAS;
   finalize_regions(b, ws);
   Desc& d = b.descs[0];
+  if (m_dtype != OCC_BF16) d.qbf = nullptr;
   d.M = M;
   d.P = P;
   d.Q = Q;

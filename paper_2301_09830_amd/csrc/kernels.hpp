@@ -110,12 +110,34 @@ __device__ __forceinline__ int find_matrix(const Desc* __restrict__ table, int c
 // ---------------------------------------------------------------------------
 // Warm-start Q -> padded layout qpad[n_pad][rp] (zeros beyond n and rank).
 // ---------------------------------------------------------------------------
+// Large-rank path with bf16 M: Q[c][k] is also kept as two bf16 parts
+// hi = bf16(v), lo = bf16(v - hi) (v - hi - lo is below 2^-16 |v|), stored
+// transposed so that the left product stages 32 columns of a rank row with
+// 16-byte copies; rank k goes to row (k % NU) * 32 + k / NU, NU = RP / 32,
+// the order in which that kernel's lanes read them.
+__device__ __forceinline__ uint16_t bf16_bits(__bf16 h) { return __builtin_bit_cast(uint16_t, h); }
+
+template <int RP>
+__device__ __forceinline__ void qbf_store(const Desc& d, int c, int k, float v) {
+  if constexpr (RP > kFusedMaxRank) {
+    if (!d.qbf) return;
+    constexpr int NU = RP / 32;
+    const int prow = (k % NU) * 32 + k / NU;
+    const __bf16 hi = (__bf16)v;
+    const __bf16 lo = (__bf16)(v - (float)hi);
+    d.qbf[(int64_t)prow * d.n_pad + c] = bf16_bits(hi);
+    d.qbf[(int64_t)(RP + prow) * d.n_pad + c] = bf16_bits(lo);
+  }
+}
+
 template <int RP>
 __device__ __forceinline__ void qpad_body(const Desc& d, int b) {
   const int64_t idx = (int64_t)b * kBlock + threadIdx.x;
   if (idx >= (int64_t)d.n_pad * RP) return;
   const int c = (int)(idx / RP), k = (int)(idx % RP);
-  d.qpad[idx] = (c < d.n && k < d.r) ? d.Q[(int64_t)c * d.r + k] : 0.f;
+  const float v = (c < d.n && k < d.r) ? d.Q[(int64_t)c * d.r + k] : 0.f;
+  d.qpad[idx] = v;
+  qbf_store<RP>(d, c, k, v);
 }
 
 template <int RP>
@@ -161,6 +183,7 @@ __device__ __forceinline__ void qred_body(const Desc& d, int b) {
   float v = d.qpart[idx];
   for (int s = 1; s < d.sq; ++s) v = v + d.qpart[(int64_t)s * d.n * RP + idx];
   d.qpad[idx] = v;
+  qbf_store<RP>(d, c, k, v);
   if (k < d.r) d.Q[(int64_t)c * d.r + k] = v;
 }
 

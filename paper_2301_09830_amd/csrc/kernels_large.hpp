@@ -39,6 +39,8 @@
 //             is staged (transposed) in LDS.
 #pragma once
 
+#include <type_traits>
+
 #include "kernels_mfma16.hpp"
 
 namespace occ {
@@ -168,14 +170,21 @@ __device__ __forceinline__ float rawa_val(const RawA<DT, SA, W>& x, int j) {
   }
 }
 
-// Store W values of A over the error buffer (row < m).
+// Store W values of A over the error buffer (row < m).  Nontemporal stores:
+// with plain stores the partially written lines were fetched before being
+// written (the first left product read 1.5 bytes for every byte of A it
+// stored, on top of M and err_prev).
 template <int W>
 __device__ __forceinline__ void a_store(const Desc& d, bool vec, int row, int c, int c_hi,
                                         const float* a) {
   if (row >= d.m) return;
   float* p = d.err_out + (int64_t)row * d.lde_out + c;
   if (vec && c + W <= c_hi) {
-    st_f<W>(p, a);
+    typedef float nt4 __attribute__((ext_vector_type(4)));
+    static_assert(W % 4 == 0, "vector A stores are whole float4s");
+#pragma unroll
+    for (int j = 0; j < W; j += 4)
+      __builtin_nontemporal_store(nt4{a[j], a[j + 1], a[j + 2], a[j + 3]}, (nt4*)(p + j));
   } else {
 #pragma unroll
     for (int j = 0; j < W; ++j)
@@ -193,17 +202,43 @@ __device__ __forceinline__ int kcol_of(int c_lo, int ks0, int it, int nk) {
 
 // -------------------------------------------------------------------------
 // k_lp: P partials = A Q for one 128-row tile and one column split.
+//
+// X3 (bf16 M): the products run on v_mfma_f32_32x32x16_bf16 with each
+// operand split in two bf16 parts, x = x_hi + x_lo (x - x_hi - x_lo is below
+// 2^-16 |x|), and A Q accumulated in fp32 as A_hi Q_hi + A_hi Q_lo +
+// A_lo Q_hi: about 1e-5 relative accuracy at 3/16 of the matrix-core cycles
+// of the fp32 v_mfma_f32_32x32x2_f32 form.  Lane (g, li) of a K-step holds
+// columns 16g..16g+15 of its row; MFMA c (0, 1) takes its columns
+// 16g + 8c .. 16g + 8c + 7 as K indices 8g..8g+7, and the B operand reads the
+// same columns of the Q tile, which is staged as bf16 hi/lo rows (one row per
+// rank, 32 columns) in the order k -> (k % NU) * 32 + k / NU so that lane li
+// of rank tile u finds rank NU li + u in row 32 u + li.
 // -------------------------------------------------------------------------
+constexpr int LB_P = L_KC + 8;   // LDS pitch (bf16) of a staged Q row: 80 bytes
+
 template <int RP>
 struct LPSmem {
   float q[2][L_KC * (RP + 4)];   // Q rows of the current and next K-step
 };
+template <int RP>
+struct LPXSmem {
+  uint16_t q[2][2][RP * LB_P];   // [stage][hi, lo][rank row][column]
+};
 
-template <int DT, int RP, int SA>
-__device__ __forceinline__ void lp_body(const Desc& d, int b, LPSmem<RP>& sm) {
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+__device__ __forceinline__ f16v mfma32bf(bf16x8 a, bf16x8 b, f16v c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+template <int DT, int RP, int SA, bool X3>
+__device__ __forceinline__ void lp_body(const Desc& d, int b,
+                                        std::conditional_t<X3, LPXSmem<RP>, LPSmem<RP>>& sm) {
   constexpr int NU = RP / 32;               // rank tiles
-  constexpr int QP = RP + 4;                // LDS pitch of a Q row
-  constexpr int QF4 = L_KC * RP / 4 / kBlock;  // float4s per thread per Q tile
+  constexpr int QP = RP + 4;                // LDS pitch of a Q row (fp32 form)
+  // 16-byte chunks of one K-step's Q tile per thread: fp32 form RP x 32 x 4 B,
+  // bf16 form 2 x RP x 32 x 2 B (the same count)
+  constexpr int QF4 = L_KC * RP / 4 / kBlock;
   static_assert(QF4 * 4 * kBlock == L_KC * RP, "Q tile must split evenly");
   const bool vec = d.vec != 0;
   const int wave = wave_id(), lane = threadIdx.x & 63;
@@ -222,11 +257,32 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b, LPSmem<RP>& sm) {
 #pragma unroll
   for (int u = 0; u < NU; ++u) acc[u] = f16v{};
 
-  // qpad has n_pad (a multiple of 32) rows, so every K-step's Q tile is in
-  // bounds; its rows past n are zero.  Q tiles are fetched LP_QAHEAD K-steps
-  // before they are needed (a register ring) and written to the LDS buffer
-  // of the next K-step at the end of each step; A loads run LP_DEPTH K-steps
-  // ahead.
+  // Source and LDS slot of this thread's chunk x of the Q tile at column c.
+  // fp32 form: qpad has n_pad (a multiple of 32) rows, so every K-step's Q
+  // tile is in bounds (rows past n are zero); bf16 form: qbf rows have n_pad
+  // columns, likewise zero past n.
+  auto q_src_ptr = [&](int c, int x) -> const f4v* {
+    const int f = threadIdx.x + kBlock * x;
+    if constexpr (X3) {
+      const int h = f / (RP * 4), rem = f % (RP * 4);
+      return (const f4v*)(d.qbf + ((int64_t)h * RP + rem / 4) * d.n_pad + c + 8 * (rem % 4));
+    } else {
+      return (const f4v*)(d.qpad + (int64_t)c * RP + 4 * f);
+    }
+  };
+  auto q_lds_ptr = [&](int stage, int x) -> f4v* {
+    const int f = threadIdx.x + kBlock * x;
+    if constexpr (X3) {
+      const int h = f / (RP * 4), rem = f % (RP * 4);
+      return (f4v*)(&sm.q[stage][h][(rem / 4) * LB_P + 8 * (rem % 4)]);
+    } else {
+      return (f4v*)(&sm.q[stage][((4 * f) / RP) * QP + (4 * f) % RP]);
+    }
+  };
+
+  // Q tiles are fetched LP_QAHEAD K-steps before they are needed (a register
+  // ring) and written to the LDS buffer of the next K-step at the end of each
+  // step; A loads run LP_DEPTH K-steps ahead.
   constexpr int LP_QAHEAD = RP >= 128 ? 1 : 3;
   constexpr int LP_DEPTH = RP >= 128 ? 2 : 1;
   f4v qr[LP_QAHEAD][QF4];
@@ -235,14 +291,10 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b, LPSmem<RP>& sm) {
     if (y < nk) {
       const int c = kcol_of(c_lo, ks0, y, nk);
 #pragma unroll
-      for (int x = 0; x < QF4; ++x)
-        qr[y][x] = *(const f4v*)(d.qpad + (int64_t)c * RP + 4 * (threadIdx.x + kBlock * x));
+      for (int x = 0; x < QF4; ++x) qr[y][x] = *q_src_ptr(c, x);
     }
 #pragma unroll
-  for (int x = 0; x < QF4; ++x) {
-    const int f = 4 * (threadIdx.x + kBlock * x);
-    *(f4v*)(&sm.q[0][(f / RP) * QP + f % RP]) = qr[0][x];
-  }
+  for (int x = 0; x < QF4; ++x) *q_lds_ptr(0, x) = qr[0][x];
   RawA<DT, SA, 16> ring[LP_DEPTH + 1];
 #pragma unroll
   for (int x = 0; x <= LP_DEPTH; ++x)
@@ -259,20 +311,43 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b, LPSmem<RP>& sm) {
     if (it + LP_QAHEAD < nk) {
       const int c = kcol_of(c_lo, ks0, it + LP_QAHEAD, nk);
 #pragma unroll
-      for (int x = 0; x < QF4; ++x)
-        qr[LP_QAHEAD - 1][x] = *(const f4v*)(d.qpad + (int64_t)c * RP + 4 * (threadIdx.x + kBlock * x));
+      for (int x = 0; x < QF4; ++x) qr[LP_QAHEAD - 1][x] = *q_src_ptr(c, x);
     }
     float a[16];
 #pragma unroll
     for (int j = 0; j < 16; ++j) a[j] = rawa_val<DT, SA, 16>(ring[0], j);
     if constexpr (SA == SA_MERR_SAVE) a_store<16>(d, vec, row, kc + 16 * g, c_hi, a);
-    const float* qb = sm.q[it & 1] + 16 * g * QP + NU * li;
+    if constexpr (X3) {
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      float bv[NU];
-      ld_f<NU>(qb + j * QP, bv);
+      for (int c = 0; c < 2; ++c) {
+        bf16x8 ahi, alo;
 #pragma unroll
-      for (int u = 0; u < NU; ++u) acc[u] = mfma32(a[j], bv[u], acc[u]);
+        for (int e = 0; e < 8; ++e) {
+          const float v = a[8 * c + e];
+          const __bf16 h = (__bf16)v;
+          ahi[e] = h;
+          alo[e] = (__bf16)(v - (float)h);
+        }
+        const uint16_t* qh = &sm.q[it & 1][0][li * LB_P + 16 * g + 8 * c];
+        const uint16_t* ql = &sm.q[it & 1][1][li * LB_P + 16 * g + 8 * c];
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+          const bf16x8 bh = *(const bf16x8*)(qh + 32 * u * LB_P);
+          const bf16x8 bl = *(const bf16x8*)(ql + 32 * u * LB_P);
+          acc[u] = mfma32bf(ahi, bh, acc[u]);
+          acc[u] = mfma32bf(ahi, bl, acc[u]);
+          acc[u] = mfma32bf(alo, bh, acc[u]);
+        }
+      }
+    } else {
+      const float* qb = sm.q[it & 1] + 16 * g * QP + NU * li;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        float bv[NU];
+        ld_f<NU>(qb + j * QP, bv);
+#pragma unroll
+        for (int u = 0; u < NU; ++u) acc[u] = mfma32(a[j], bv[u], acc[u]);
+      }
     }
 #pragma unroll
     for (int x = 0; x < LP_DEPTH; ++x) ring[x] = ring[x + 1];
@@ -281,10 +356,7 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b, LPSmem<RP>& sm) {
     if (it + 1 < nk) {
       // slot 0 now holds K-step it + 1
 #pragma unroll
-      for (int x = 0; x < QF4; ++x) {
-        const int f = 4 * (threadIdx.x + kBlock * x);
-        *(f4v*)(&sm.q[(it + 1) & 1][(f / RP) * QP + f % RP]) = qr[0][x];
-      }
+      for (int x = 0; x < QF4; ++x) *q_lds_ptr((it + 1) & 1, x) = qr[0][x];
       kc = kcol_of(c_lo, ks0, it + 1, nk);
     }
     __syncthreads();
@@ -304,10 +376,10 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b, LPSmem<RP>& sm) {
   }
 }
 
-template <int DT, int RP, int SA>
+template <int DT, int RP, int SA, bool X3>
 __global__ __launch_bounds__(kBlock) void k_lp(OCC_KARGS) {
-  __shared__ __attribute__((aligned(16))) LPSmem<RP> sm;
-#define B_(d, b) lp_body<DT, RP, SA>(d, b, sm)
+  __shared__ __attribute__((aligned(16))) std::conditional_t<X3, LPXSmem<RP>, LPSmem<RP>> sm;
+#define B_(d, b) lp_body<DT, RP, SA, X3>(d, b, sm)
   OCC_DISPATCH(K_PASS_P, B_)
 #undef B_
 }
@@ -741,6 +813,169 @@ template <int DT, int RP, int SA>
 __global__ __launch_bounds__(kBlock) void k_lq(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) LQSmem<RP> sm;
 #define B_(d, b) lq_body<DT, RP, SA>(d, b, sm)
+  OCC_DISPATCH(K_PASS_Q, B_)
+#undef B_
+}
+
+// -------------------------------------------------------------------------
+// k_lqx: the right product for bf16 M on the bf16 matrix cores, with split
+// operands as in k_lp (X3): Q^T partial = P_hat^T A over 16-row groups, as
+// v_mfma_f32_32x32x16_bf16 with
+//   A operand  P_hat^T: lane (g, li) supplies rank 32u + li, rows 8g..8g+7 of
+//              the group, from an LDS tile of bf16 hi/lo rows (16 rows per
+//              rank) staged from the transposed P_hat (phat_t);
+//   B operand  A: lane (g, li) supplies rows 8g..8g+7 of its column
+//              ct*BC + 32*CPL*w + CPL*li + x (the same 2-row x 32-lane loads
+//              as k_lq);
+// so acc[x][u][v] = Q[col][rank 32u + mf32_row(v, g)] of this split.
+// -------------------------------------------------------------------------
+constexpr int LQX_G = 16;            // rows per group (K of two MFMA halves)
+constexpr int LQX_P = LQX_G + 8;     // LDS pitch (bf16) of a staged rank row: 48 bytes
+
+template <int RP>
+struct LQXSmem {
+  uint16_t p[2][2][RP * LQX_P];      // [stage][hi, lo][rank][row]
+};
+
+template <int DT, int RP, int SA>
+__device__ __forceinline__ void lqx_body(const Desc& d, int b, LQXSmem<RP>& sm) {
+  constexpr int NU = RP / 32, CPL = lq_cpl(RP), BC = lq_block_cols(RP);
+  constexpr int NCH = RP * LQX_G / 4;                 // float4 chunks of a P_hat tile
+  constexpr int PFX = (NCH + kBlock - 1) / kBlock;    // per thread
+  constexpr int LQX_PAHEAD = 2;                        // P_hat groups fetched ahead
+  const bool vec = d.vec != 0;
+  const int wave = wave_id(), lane = threadIdx.x & 63;
+  const int li = lane & 31, g = lane >> 5;
+  const int t = threadIdx.x;
+  const int col_tiles = (d.n + BC - 1) / BC;
+  const int ct = b % col_tiles, s = b / col_tiles;
+  const int cw = ct * BC + wave * 32 * CPL;
+  const int col = cw + CPL * li;
+  const int r_lo = s * d.q_rows, r_hi = min(d.m, r_lo + d.q_rows);
+  const int ngrp = (r_hi - r_lo + LQX_G - 1) / LQX_G;
+
+  f16v acc[CPL][NU];
+#pragma unroll
+  for (int x = 0; x < CPL; ++x)
+#pragma unroll
+    for (int u = 0; u < NU; ++u) acc[x][u] = f16v{};
+
+  // P_hat^T chunk f of group grp: rank f / 4, rows r0 + 4 (f % 4) .. + 3
+  // (zero at rows >= r_hi; phat_t rows are m_pad long and the chunks start
+  // at multiples of 4 rows, so a chunk that starts below r_hi is in bounds)
+  auto p_fetch = [&](int grp, f4v* pr) {
+    const int r0 = r_lo + LQX_G * grp;
+#pragma unroll
+    for (int x = 0; x < PFX; ++x) {
+      const int f = t + kBlock * x;
+      pr[x] = f4v{0.f, 0.f, 0.f, 0.f};
+      const int row = r0 + 4 * (f % 4);
+      if (f < NCH && grp < ngrp && row < r_hi) {
+        pr[x] = *(const f4v*)(d.phat_t + (int64_t)(f / 4) * d.m_pad + row);
+#pragma unroll
+        for (int e = 1; e < 4; ++e)
+          if (row + e >= r_hi) pr[x][e] = 0.f;
+      }
+    }
+  };
+  auto p_stage = [&](int stage, const f4v* pr) {
+#pragma unroll
+    for (int x = 0; x < PFX; ++x) {
+      const int f = t + kBlock * x;
+      if (f < NCH) {
+        uint16_t hi[4], lo[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const __bf16 h = (__bf16)pr[x][e];
+          hi[e] = bf16_bits(h);
+          lo[e] = bf16_bits((__bf16)(pr[x][e] - (float)h));
+        }
+        const int off = (f / 4) * LQX_P + 4 * (f % 4);
+        *(uint2*)(&sm.p[stage][0][off]) = make_uint2(hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
+        *(uint2*)(&sm.p[stage][1][off]) = make_uint2(lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16));
+      }
+    }
+  };
+  auto a_fetch = [&](int grp, RawA<DT, SA, CPL>* x) {
+    const int r0 = r_lo + LQX_G * grp;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int row = r0 + 8 * g + e;
+      x[e] = rawa_load<DT, SA, CPL>(d, vec, row < r_hi ? row : d.m, col, d.n);
+    }
+  };
+
+  // A groups are fetched LQX_ADEPTH groups ahead (a register ring), P_hat
+  // chunks LQX_PAHEAD groups ahead and staged in LDS one group ahead.
+  constexpr int LQX_ADEPTH = CPL >= 4 ? 1 : 2;
+  f4v pr[LQX_PAHEAD][PFX];
+#pragma unroll
+  for (int y = 0; y < LQX_PAHEAD; ++y) p_fetch(y, pr[y]);
+  p_stage(0, pr[0]);
+  RawA<DT, SA, CPL> ring[LQX_ADEPTH + 1][8];
+#pragma unroll
+  for (int y = 0; y <= LQX_ADEPTH; ++y)
+    if (y < ngrp) a_fetch(y, ring[y]);
+  __syncthreads();
+
+  for (int grp = 0; grp < ngrp; ++grp) {
+    const bool more = grp + 1 < ngrp;
+#pragma unroll
+    for (int y = 0; y + 1 < LQX_PAHEAD; ++y)
+#pragma unroll
+      for (int x = 0; x < PFX; ++x) pr[y][x] = pr[y + 1][x];
+    p_fetch(grp + LQX_PAHEAD, pr[LQX_PAHEAD - 1]);
+    const uint16_t* ph = &sm.p[grp & 1][0][li * LQX_P + 8 * g];
+    const uint16_t* pl = &sm.p[grp & 1][1][li * LQX_P + 8 * g];
+#pragma unroll
+    for (int x = 0; x < CPL; ++x) {
+      bf16x8 bh, bl;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float v = rawa_val<DT, SA, CPL>(ring[0][e], x);
+        const __bf16 h = (__bf16)v;
+        bh[e] = h;
+        bl[e] = (__bf16)(v - (float)h);
+      }
+#pragma unroll
+      for (int u = 0; u < NU; ++u) {
+        const bf16x8 ah = *(const bf16x8*)(ph + 32 * u * LQX_P);
+        const bf16x8 al = *(const bf16x8*)(pl + 32 * u * LQX_P);
+        acc[x][u] = mfma32bf(ah, bh, acc[x][u]);
+        acc[x][u] = mfma32bf(ah, bl, acc[x][u]);
+        acc[x][u] = mfma32bf(al, bh, acc[x][u]);
+      }
+    }
+#pragma unroll
+    for (int y = 0; y < LQX_ADEPTH; ++y)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ring[y][e] = ring[y + 1][e];
+    if (grp + LQX_ADEPTH + 1 < ngrp) a_fetch(grp + LQX_ADEPTH + 1, ring[LQX_ADEPTH]);
+    // slot 0 now holds group grp + 1
+    if (more) p_stage((grp + 1) & 1, pr[0]);
+    __syncthreads();
+  }
+
+  // acc[x][u][4q + w] = Q[col + x][rank 32u + 8q + 4g + w] (this split)
+#pragma unroll
+  for (int x = 0; x < CPL; ++x) {
+    const int c = col + x;
+    if (c < d.n) {
+      float* dst = d.qpart + ((int64_t)s * d.n + c) * RP;
+#pragma unroll
+      for (int u = 0; u < NU; ++u)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          *(float4*)(dst + 32 * u + 8 * q + 4 * g) =
+              make_float4(acc[x][u][4 * q], acc[x][u][4 * q + 1], acc[x][u][4 * q + 2], acc[x][u][4 * q + 3]);
+    }
+  }
+}
+
+template <int DT, int RP, int SA>
+__global__ __launch_bounds__(kBlock) void k_lqx(OCC_KARGS) {
+  __shared__ __attribute__((aligned(16))) LQXSmem<RP> sm;
+#define B_(d, b) lqx_body<DT, RP, SA>(d, b, sm)
   OCC_DISPATCH(K_PASS_Q, B_)
 #undef B_
 }

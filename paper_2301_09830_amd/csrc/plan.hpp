@@ -52,6 +52,8 @@ struct Desc {
   double* tm;            // rp x rp (large-rank path: T2 of the second pass)
   uint32_t* info;        // [0] = second CholeskyQR pass needed
   float* phat_t;         // large-rank path: P_hat transposed, rp x m_pad
+  uint16_t* qbf;         // large-rank path, bf16 M: Q as bf16 hi/lo parts, [2][rp][n_pad],
+                         // rank k in row (k % (rp/32)) * 32 + k / (rp/32)
   // shapes
   int32_t m, n, r;
   int32_t ldm, lde_in, lde_out, ldh;
@@ -184,7 +186,7 @@ constexpr size_t kAlign = 256;
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Regions {
-  size_t qpad, phat, praw, ppart, qpart, gpart, gsum, t1, tm, info, phat_t, total;
+  size_t qpad, phat, praw, ppart, qpart, gpart, gsum, t1, tm, info, phat_t, qbf, total;
 };
 
 inline Regions matrix_regions(int64_t m, int64_t n, int rp, const Tiling& t) {
@@ -202,6 +204,7 @@ inline Regions matrix_regions(int64_t m, int64_t n, int rp, const Tiling& t) {
   g.tm = take((size_t)rp * rp * 8);
   g.info = take(64);
   g.phat_t = take(rp > kFusedMaxRank ? (size_t)rp * t.m_pad * 4 : 0);
+  g.qbf = take(rp > kFusedMaxRank ? (size_t)2 * rp * t.n_pad * 2 : 0);
   g.total = off;
   return g;
 }
