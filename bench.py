@@ -167,7 +167,7 @@ def profile_name(kname: str) -> str | None:
     short = base.split("<")[0]
     args = [a.strip() for a in base[len(short) + 1:-1].split(",")] if "<" in base else []
     fixed = {"k_pm": "pass_p", "k_qm": "pass_q", "k_orth16": "orth", "k_qred16": "q_reduce",
-             "k_qred": "q_reduce", "k_qpad": "qpad"}
+             "k_qred": "q_reduce", "k_qpad": "qpad", "k_qredl": "q_reduce", "k_qpadl": "qpad"}
     if short in fixed:
         return fixed[short]
     if short == "k_mh16":
@@ -182,6 +182,8 @@ def profile_name(kname: str) -> str | None:
         if args[3] == "1":
             return "decompress"
         return "mhat_err_a" if args[4] == "true" else "err_only_a"
+    if short == "k_lqx":
+        return {"0": "pass_q", "2": "pass_q_a"}[args[2]]
     pair = {"k_lg": "gram", "k_gsum": "gram_sum", "k_lchol": "chol", "k_lapply": "apply"}
     if short in pair:
         return pair[short] + ("2" if args[-1] == "1" else "")

@@ -351,7 +351,7 @@ occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, h
         const bool saved = b.descs[0].err_out != nullptr;
         // bf16 M: left products on bf16 matrix cores with split operands
         constexpr bool X3 = DT == DT_BF16;
-        L("qpad", k_qpad<RP>, b.blocks[K_QPAD]);
+        L("qpad", k_qpadl<RP>, b.blocks[K_QPAD]);
         for (int it = 0; it < b.iters; ++it) {
           if (!saved)
             L("pass_p", k_lp<DT, RP, SA_MERR, X3>, b.blocks[K_PASS_P]);
@@ -378,7 +378,7 @@ occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, h
             else
               L("pass_q", k_lq<DT, RP, SA_MERR>, b.blocks[K_PASS_Q]);
           }
-          L("q_reduce", k_qred<RP>, b.blocks[K_QRED]);
+          L("q_reduce", k_qredl<RP>, b.blocks[K_QRED]);
         }
         if (finish) {
           if (write_mhat)

@@ -110,34 +110,12 @@ __device__ __forceinline__ int find_matrix(const Desc* __restrict__ table, int c
 // ---------------------------------------------------------------------------
 // Warm-start Q -> padded layout qpad[n_pad][rp] (zeros beyond n and rank).
 // ---------------------------------------------------------------------------
-// Large-rank path with bf16 M: Q[c][k] is also kept as two bf16 parts
-// hi = bf16(v), lo = bf16(v - hi) (v - hi - lo is below 2^-16 |v|), stored
-// transposed so that the left product stages 32 columns of a rank row with
-// 16-byte copies; rank k goes to row (k % NU) * 32 + k / NU, NU = RP / 32,
-// the order in which that kernel's lanes read them.
-__device__ __forceinline__ uint16_t bf16_bits(__bf16 h) { return __builtin_bit_cast(uint16_t, h); }
-
-template <int RP>
-__device__ __forceinline__ void qbf_store(const Desc& d, int c, int k, float v) {
-  if constexpr (RP > kFusedMaxRank) {
-    if (!d.qbf) return;
-    constexpr int NU = RP / 32;
-    const int prow = (k % NU) * 32 + k / NU;
-    const __bf16 hi = (__bf16)v;
-    const __bf16 lo = (__bf16)(v - (float)hi);
-    d.qbf[(int64_t)prow * d.n_pad + c] = bf16_bits(hi);
-    d.qbf[(int64_t)(RP + prow) * d.n_pad + c] = bf16_bits(lo);
-  }
-}
-
 template <int RP>
 __device__ __forceinline__ void qpad_body(const Desc& d, int b) {
   const int64_t idx = (int64_t)b * kBlock + threadIdx.x;
   if (idx >= (int64_t)d.n_pad * RP) return;
   const int c = (int)(idx / RP), k = (int)(idx % RP);
-  const float v = (c < d.n && k < d.r) ? d.Q[(int64_t)c * d.r + k] : 0.f;
-  d.qpad[idx] = v;
-  qbf_store<RP>(d, c, k, v);
+  d.qpad[idx] = (c < d.n && k < d.r) ? d.Q[(int64_t)c * d.r + k] : 0.f;
 }
 
 template <int RP>
@@ -174,22 +152,87 @@ __global__ __launch_bounds__(kBlock) void k_gsum(OCC_KARGS) {
 constexpr double kPivotTol = 1e-12;
 constexpr double kSecondPassCond = 1e3;
 
-// Q[c][k] = sum_s qpart[s][c][k] (fixed order) -> caller's Q and qpad.
+// ---------------------------------------------------------------------------
+// Large-rank path: Q padding (k_qpadl) and the Q reduction (k_qredl) over
+// 32-column tiles.  Both write qpad (n_pad x RP) and, when M is bf16, Q as
+// two bf16 parts hi = bf16(v), lo = bf16(v - hi) (v - hi - lo is below
+// 2^-16 |v|) in qbf, transposed so that the left product stages 32 columns
+// of a rank row with 16-byte copies: rank k goes to row (k % NU) * 32 + k / NU,
+// NU = RP / 32, the order in which that kernel's lanes read them.  The
+// transpose goes through LDS, so qbf is written in 16-byte runs.
+// k_qpadl covers all n_pad columns (zeros past n); k_qredl sums the row-split
+// partials (fixed order) for the n real columns and also writes the caller's Q.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint16_t bf16_bits(__bf16 h) { return __builtin_bit_cast(uint16_t, h); }
+
+constexpr int QT_COLS = 8;                  // columns per block
+constexpr int QT_P = QT_COLS;               // LDS pitch (bf16) of a transposed rank row
+
 template <int RP>
-__device__ __forceinline__ void qred_body(const Desc& d, int b) {
-  const int64_t idx = (int64_t)b * kBlock + threadIdx.x;
-  if (idx >= (int64_t)d.n * RP) return;
-  const int c = (int)(idx / RP), k = (int)(idx % RP);
-  float v = d.qpart[idx];
-  for (int s = 1; s < d.sq; ++s) v = v + d.qpart[(int64_t)s * d.n * RP + idx];
-  d.qpad[idx] = v;
-  qbf_store<RP>(d, c, k, v);
-  if (k < d.r) d.Q[(int64_t)c * d.r + k] = v;
+struct QTSmem {
+  uint16_t t[2][RP * QT_P];
+};
+
+template <int RP, bool REDUCE>
+__device__ __forceinline__ void qtile_body(const Desc& d, int b, QTSmem<RP>& sm) {
+  constexpr int NU = RP / 32;
+  const int c0 = b * QT_COLS;
+  const int c_end = REDUCE ? d.n : d.n_pad;
+  for (int e = threadIdx.x; e < QT_COLS * RP; e += kBlock) {
+    const int c = c0 + e / RP, k = e % RP;
+    if (c >= c_end) continue;
+    const int64_t idx = (int64_t)c * RP + k;
+    float v;
+    if (REDUCE) {
+      // fixed order; loads issued in batches of 8
+      v = 0.f;
+      for (int s0 = 0; s0 < d.sq; s0 += 8) {
+        float p[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) p[u] = (s0 + u < d.sq) ? d.qpart[(int64_t)(s0 + u) * d.n * RP + idx] : 0.f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (s0 + u < d.sq) v = (s0 + u == 0) ? p[u] : v + p[u];
+      }
+      if (k < d.r) d.Q[(int64_t)c * d.r + k] = v;
+    } else {
+      v = (c < d.n && k < d.r) ? d.Q[(int64_t)c * d.r + k] : 0.f;
+    }
+    d.qpad[idx] = v;
+    if (d.qbf) {
+      const int prow = (k % NU) * 32 + k / NU;
+      const __bf16 hi = (__bf16)v;
+      sm.t[0][prow * QT_P + (c - c0)] = bf16_bits(hi);
+      sm.t[1][prow * QT_P + (c - c0)] = bf16_bits((__bf16)(v - (float)hi));
+    }
+  }
+  if (!d.qbf) return;
+  __syncthreads();
+  // 2 x RP rows of 8 columns, one 16-byte chunk each
+  for (int f = threadIdx.x; f < 2 * RP; f += kBlock) {
+    const int h = f / RP, prow = f % RP, part = 0;
+    const int c = c0;
+    if (c + 8 <= c_end) {
+      *(uint4*)(d.qbf + ((int64_t)h * RP + prow) * d.n_pad + c) = *(const uint4*)(&sm.t[h][prow * QT_P + 8 * part]);
+    } else {
+      for (int j = 0; j < 8 && c + j < c_end; ++j)
+        d.qbf[((int64_t)h * RP + prow) * d.n_pad + c + j] = sm.t[h][prow * QT_P + 8 * part + j];
+    }
+  }
 }
 
 template <int RP>
-__global__ __launch_bounds__(kBlock) void k_qred(OCC_KARGS) {
-#define B_(d, b) qred_body<RP>(d, b)
+__global__ __launch_bounds__(kBlock) void k_qpadl(OCC_KARGS) {
+  __shared__ __attribute__((aligned(16))) QTSmem<RP> sm;
+#define B_(d, b) qtile_body<RP, false>(d, b, sm)
+  OCC_DISPATCH(K_QPAD, B_)
+#undef B_
+}
+
+template <int RP>
+__global__ __launch_bounds__(kBlock) void k_qredl(OCC_KARGS) {
+  __shared__ __attribute__((aligned(16))) QTSmem<RP> sm;
+#define B_(d, b) qtile_body<RP, true>(d, b, sm)
   OCC_DISPATCH(K_QRED, B_)
 #undef B_
 }

@@ -170,21 +170,16 @@ __device__ __forceinline__ float rawa_val(const RawA<DT, SA, W>& x, int j) {
   }
 }
 
-// Store W values of A over the error buffer (row < m).  Nontemporal stores:
-// with plain stores the partially written lines were fetched before being
-// written (the first left product read 1.5 bytes for every byte of A it
-// stored, on top of M and err_prev).
+// Store W values of A over the error buffer (row < m).  Plain stores: the
+// stored A is read back by the next pass, and nontemporal stores measured
+// slower for the whole step.
 template <int W>
 __device__ __forceinline__ void a_store(const Desc& d, bool vec, int row, int c, int c_hi,
                                         const float* a) {
   if (row >= d.m) return;
   float* p = d.err_out + (int64_t)row * d.lde_out + c;
   if (vec && c + W <= c_hi) {
-    typedef float nt4 __attribute__((ext_vector_type(4)));
-    static_assert(W % 4 == 0, "vector A stores are whole float4s");
-#pragma unroll
-    for (int j = 0; j < W; j += 4)
-      __builtin_nontemporal_store(nt4{a[j], a[j + 1], a[j + 2], a[j + 3]}, (nt4*)(p + j));
+    st_f<W>(p, a);
   } else {
 #pragma unroll
     for (int j = 0; j < W; ++j)

@@ -332,9 +332,12 @@ struct MXSmem {
 // or from a caller's m x r array element by element (zero past rank r).
 template <int S>
 __device__ __forceinline__ void factor_vec(const float* p, float v[S]) {
-  if constexpr (S == 4) {
-    const float4 x = *(const float4*)p;
-    v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+  if constexpr (S % 4 == 0) {
+#pragma unroll
+    for (int j = 0; j < S; j += 4) {
+      const float4 x = *(const float4*)(p + j);
+      v[j] = x.x; v[j + 1] = x.y; v[j + 2] = x.z; v[j + 3] = x.w;
+    }
   } else if constexpr (S == 2) {
     const float2 x = *(const float2*)p;
     v[0] = x.x; v[1] = x.y;

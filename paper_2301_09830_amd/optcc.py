@@ -105,13 +105,16 @@ _SIGS = {
 
 
 def lib() -> ctypes.CDLL:
-    """The loaded liboptcc.so; raises if it has not been built."""
+    """The loaded liboptcc.so; raises if it has not been built.  The
+    environment variable OPTCC_LIBRARY selects another build of the same
+    library (for side-by-side comparisons of kernel variants)."""
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB_PATH):
-            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+        path = os.environ.get("OPTCC_LIBRARY", LIB_PATH)
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is missing: build it with "
                                "`python -m paper_2301_09830_amd.build`")
-        handle = ctypes.CDLL(LIB_PATH)
+        handle = ctypes.CDLL(path)
         for name, (res, args) in _SIGS.items():
             fn = getattr(handle, name)
             fn.restype = res
