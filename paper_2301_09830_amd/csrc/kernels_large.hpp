@@ -902,7 +902,7 @@ __device__ __forceinline__ void lqx_body(const Desc& d, int b, LQXSmem<RP>& sm) 
 
   // A groups are fetched LQX_ADEPTH groups ahead (a register ring), P_hat
   // chunks LQX_PAHEAD groups ahead and staged in LDS one group ahead.
-  constexpr int LQX_ADEPTH = CPL >= 4 ? 1 : 2;
+  constexpr int LQX_ADEPTH = CPL >= 4 ? 1 : 2;   // 1 and 4 measured slower at rank 128
   f4v pr[LQX_PAHEAD][PFX];
 #pragma unroll
   for (int y = 0; y < LQX_PAHEAD; ++y) p_fetch(y, pr[y]);

@@ -100,3 +100,22 @@ def test_unaligned_leading_dimension():
     wb = WORKLOADS[2].scaled([(130, 75)], rank=8)
     res, _, _ = run_workload(wb, 2, ld_pad=3)
     assert_parity(res, "bf16", "bf16 ld = n + 3 (scalar path)")
+
+
+@pytest.mark.parametrize("snr", [False, True])
+@pytest.mark.parametrize("rank", [32, 64, 128])
+def test_bf16_large_rank_split_products_accuracy(rank, snr):
+    """bf16 M at rank > 16 runs its left and right products on the bf16 matrix
+    cores with each operand split as x = x_hi + x_lo (x - x_hi - x_lo below
+    2^-16 |x|).  The split must keep the result close to fp32 arithmetic:
+    measured 1e-5 (noise-dominated) to 7e-5 (high SNR, where err is 1 % of A)
+    against the float64 oracle.  Dropping the lo parts would leave bf16
+    operands (2^-9 relative), about 2e-3 per product, so the bound 5e-4 -- well
+    inside the 2e-2 bf16 tolerance -- catches a broken split."""
+    w = WORKLOADS[5].scaled([(700, 520)], rank=rank, signal_rank=160)
+    if snr:
+        w = high_snr(w)
+    res, _, _ = run_workload(w, 2)
+    worst = max(max(r["mhat"], r["err"]) for step in res for r in step)
+    print(f"[split] bf16 700x520 rank {rank} high_snr={snr}: worst rel_F = {worst:.3e}", flush=True)
+    assert worst <= 5e-4
