@@ -125,16 +125,47 @@ __global__ __launch_bounds__(kBlock) void k_qpad(OCC_KARGS) {
 #undef B_
 }
 
-// gsum[k][l] = sum_b gpart[b][k][l], fixed order (MODE 1: second CholeskyQR
-// pass, skipped unless the first pass asked for it).
+// gsum[k][l] = sum_b gpart[b][k][l] for k <= l (fixed order), zero below the
+// diagonal (the Gram partials hold the upper triangle only).  MODE 1: second
+// CholeskyQR pass, skipped unless the first pass asked for it.  A block
+// takes GS_ENT entries; GS_SL threads per entry sum interleaved slices of
+// the partials with their loads issued in batches of 8, and the slices are
+// added in slice order.
+constexpr int GS_SL = 8;
+constexpr int GS_ENT = kBlock / GS_SL;
+
 template <int RP, int MODE>
 __device__ __forceinline__ void gsum_body(const Desc& d, int b) {
   if (MODE == 1 && !d.info[0]) return;
-  const int idx = b * kBlock + threadIdx.x;
-  if (idx >= RP * RP) return;
-  double s = d.gpart[idx];
-  for (int g = 1; g < d.ng; ++g) s += d.gpart[(int64_t)g * RP * RP + idx];
-  d.gsum[idx] = s;
+  __shared__ double part[GS_SL][GS_ENT];
+  const int sl = threadIdx.x / GS_ENT, el = threadIdx.x % GS_ENT;
+  const int idx = b * GS_ENT + el;
+  const int k = idx / RP, l = idx % RP;
+  const bool upper = idx < RP * RP && k <= l;
+  double s = 0.0;
+  if (upper) {
+    for (int g0 = sl; g0 < d.ng; g0 += 8 * GS_SL) {
+      double v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int g = g0 + GS_SL * u;
+        v[u] = (g < d.ng) ? d.gpart[(int64_t)g * RP * RP + idx] : 0.0;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (g0 + GS_SL * u < d.ng) s = (g0 + GS_SL * u == sl) ? v[u] : s + v[u];
+    }
+  }
+  part[sl][el] = s;
+  __syncthreads();
+  if (sl == 0 && idx < RP * RP) {
+    double tot = 0.0;
+    if (upper) {
+      tot = part[0][el];
+      for (int x = 1; x < GS_SL && x < d.ng; ++x) tot += part[x][el];
+    }
+    d.gsum[idx] = tot;
+  }
 }
 
 template <int RP, int MODE>

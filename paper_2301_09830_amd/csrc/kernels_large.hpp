@@ -383,62 +383,121 @@ __global__ __launch_bounds__(kBlock) void k_lp(OCC_KARGS) {
 // k_lg: Gram partial of 256 rows in fp64.  MODE 0: the rows are P (sum of
 // the left product's column splits, stored to praw).  MODE 1 (second
 // CholeskyQR pass, skipped unless the first pass asked for it): the rows
-// are the first pass's P_hat.  Each thread owns an (RP/16)^2 tile of G.
+// are the first pass's P_hat.  Rows are staged in LDS as doubles, 32 at a
+// time; the upper-triangle 16 x 16 tiles of G (ta <= tb) are shared out
+// over the four waves and accumulated on v_mfma_f64_16x16x4f64, four rows
+// per instruction: lane (q, li) supplies P[row 4s + q][16 ta + li] (A
+// operand) and P[row 4s + q][16 tb + li] (B operand) and ends with
+// G[16 ta + 4v + q][16 tb + li] in component v.  Only the upper tiles are
+// written; the Gram sum zeroes the lower triangle (the Cholesky reads only
+// the upper one).
 // -------------------------------------------------------------------------
+typedef double d4v __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ d4v mfma64(double a, double b, d4v c) {
+  return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+}
+
 template <int RP>
 struct LGSmem {
   double rows[32][RP + 2];
 };
 
+// upper-triangle tiles of an NTT x NTT tile grid, in row-major order
+__host__ __device__ constexpr int lg_ntiles(int rp) { return (rp / 16) * (rp / 16 + 1) / 2; }
+__host__ __device__ constexpr int lg_per_wave(int rp) { return (lg_ntiles(rp) + 3) / 4; }
+
 template <int RP, int MODE>
 __device__ __forceinline__ void lg_body(const Desc& d, int b, LGSmem<RP>& sm) {
   if (MODE == 1 && !d.info[0]) return;
-  constexpr int TS = RP / 16;
-  const int t = threadIdx.x, ta = t >> 4, tb = t & 15;
-  double acc[TS][TS];
+  constexpr int NTT = RP / 16, NTL = lg_ntiles(RP), PW = lg_per_wave(RP);
+  const int t = threadIdx.x;
+  const int wave = wave_id(), lane = t & 63;
+  const int q = lane >> 4, li = lane & 15;
+  // this wave's tiles: indices wave, wave + 4, ... of the upper triangle
+  int ta[PW], tb[PW];
 #pragma unroll
-  for (int p = 0; p < TS; ++p)
+  for (int x = 0; x < PW; ++x) {
+    int idx = wave + 4 * x, r = 0;
+    if (idx >= NTL) idx = NTL - 1;   // padding slot (not written)
+    while (idx >= NTT - r) { idx -= NTT - r; ++r; }
+    ta[x] = r;
+    tb[x] = r + idx;
+  }
+  d4v acc[PW];
 #pragma unroll
-    for (int q = 0; q < TS; ++q) acc[p][q] = 0.0;
+  for (int x = 0; x < PW; ++x) acc[x] = d4v{0.0, 0.0, 0.0, 0.0};
+  // Staging: thread t owns float4 e of each 32-row chunk (E4 per thread).
+  // The next chunk's loads (the first LG_PB column splits in MODE 0) are
+  // issued before the current chunk's products so their latency overlaps
+  // them; further splits are added after, in split order.
+  constexpr int E4 = 32 * RP / 4 / kBlock;
+  constexpr int LG_PB = 4;
+  static_assert(E4 >= 1 && 32 * RP / 4 == E4 * kBlock, "staging layout");
   const int r_lo = b * L_GROWS, r_hi = min(d.m, r_lo + L_GROWS);
-  for (int c0 = r_lo; c0 < r_hi; c0 += 32) {
-    const int nr = min(32, r_hi - c0);
-    for (int idx = t; idx < 32 * RP; idx += kBlock) {
-      const int i = idx / RP, k = idx % RP;
-      double v = 0.0;
-      if (i < nr) {
-        const int64_t row = c0 + i;
-        if (MODE == 0) {
-          float s = d.ppart[row * RP + k];
-          for (int p = 1; p < d.sp; ++p) s = s + d.ppart[((int64_t)p * d.m + row) * RP + k];
-          d.praw[row * RP + k] = s;
-          v = (double)s;
-        } else {
-          v = (double)d.phat[row * RP + k];
+  float4 pre[E4][LG_PB];
+  auto fetch = [&](int c0) {
+#pragma unroll
+    for (int e = 0; e < E4; ++e) {
+      const int idx = t + kBlock * e, i = idx / (RP / 4), k4 = idx % (RP / 4);
+      const int64_t row = c0 + i;
+#pragma unroll
+      for (int p = 0; p < LG_PB; ++p) {
+        pre[e][p] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (row < r_hi && (p == 0 || (MODE == 0 && p < d.sp))) {
+          const float* base = MODE == 0 ? d.ppart + ((int64_t)p * d.m + row) * RP : d.phat + row * RP;
+          pre[e][p] = *(const float4*)(base + 4 * k4);
         }
       }
-      sm.rows[i][k] = v;
     }
-    __syncthreads();
-    for (int i = 0; i < nr; ++i) {
-      double x[TS], y[TS];
+  };
+  auto stage = [&](int c0) {
 #pragma unroll
-      for (int q = 0; q < TS; ++q) {
-        x[q] = sm.rows[i][TS * ta + q];
-        y[q] = sm.rows[i][TS * tb + q];
+    for (int e = 0; e < E4; ++e) {
+      const int idx = t + kBlock * e, i = idx / (RP / 4), k4 = idx % (RP / 4);
+      const int64_t row = c0 + i;
+      float4 v = pre[e][0];
+      if (MODE == 0 && row < r_hi) {
+#pragma unroll
+        for (int p = 1; p < LG_PB; ++p)
+          if (p < d.sp) v = make_float4(v.x + pre[e][p].x, v.y + pre[e][p].y, v.z + pre[e][p].z,
+                                        v.w + pre[e][p].w);
+        for (int p = LG_PB; p < d.sp; ++p) {
+          const float4 w = *(const float4*)(d.ppart + ((int64_t)p * d.m + row) * RP + 4 * k4);
+          v = make_float4(v.x + w.x, v.y + w.y, v.z + w.z, v.w + w.w);
+        }
+        *(float4*)(d.praw + row * RP + 4 * k4) = v;
       }
+      double2* dst = (double2*)&sm.rows[i][4 * k4];
+      dst[0] = make_double2((double)v.x, (double)v.y);
+      dst[1] = make_double2((double)v.z, (double)v.w);
+    }
+  };
+  fetch(r_lo);
+  for (int c0 = r_lo; c0 < r_hi; c0 += 32) {
+    stage(c0);
+    __syncthreads();
+    if (c0 + 32 < r_hi) fetch(c0 + 32);
+
+#pragma unroll 2
+    for (int s4 = 0; s4 < 8; ++s4) {
+      const double* rowp = sm.rows[4 * s4 + q];
 #pragma unroll
-      for (int p = 0; p < TS; ++p)
-#pragma unroll
-        for (int q = 0; q < TS; ++q) acc[p][q] = fma(x[p], y[q], acc[p][q]);
+      for (int x = 0; x < PW; ++x) {
+        const double av = rowp[16 * ta[x] + li];
+        const double bv = rowp[16 * tb[x] + li];
+        acc[x] = mfma64(av, bv, acc[x]);
+      }
     }
     __syncthreads();
   }
   double* gp = d.gpart + (int64_t)b * RP * RP;
 #pragma unroll
-  for (int p = 0; p < TS; ++p)
+  for (int x = 0; x < PW; ++x) {
+    if (wave + 4 * x >= NTL) continue;
 #pragma unroll
-    for (int q = 0; q < TS; ++q) gp[(TS * ta + p) * RP + TS * tb + q] = acc[p][q];
+    for (int v = 0; v < 4; ++v) gp[(16 * ta[x] + 4 * v + q) * RP + 16 * tb[x] + li] = acc[x][v];
+  }
 }
 
 template <int RP, int MODE>
@@ -451,56 +510,89 @@ __global__ __launch_bounds__(kBlock) void k_lg(OCC_KARGS) {
 
 // -------------------------------------------------------------------------
 // k_lchol: T = R^-1 with G = R^T R (fp64), one block of 1024 threads per
-// matrix.  Thread (bi, bk) keeps the (RP/32)^2 blocks of the working Gram W
-// (upper triangle) and of T at rows RP/32*bi.., columns RP/32*bk.. in
-// registers.  Step j: the owners publish row j of W and column j of T
-// through LDS, then every thread applies
-//   W[i][k] -= W[j][i] W[j][k] / W[j][j]      (j < i <= k)
-//   T[l][k] -= T[l][j] W[j][k] / W[j][j]      (l <= j < k)
-// which is the right-looking Cholesky of G together with the column
-// recurrence of its inverse factor; finally T[:, k] /= sqrt(pivot k).
-// A pivot <= kPivotTol * max diag(G), or a padding column (k >= r), is
-// dependent: its column of T is zero and it updates nothing.
+// matrix, blocked in 16 x 16 tiles (NB = RP/16 tile rows, tiles of the
+// upper triangle only, held in LDS).  Step j:
+//   1. wave 0 factors the diagonal tile W_jj = R_jj^T R_jj with the
+//      right-looking column recurrence (Cholesky of W_jj together with the
+//      column recurrence of its inverse factor; row j of W and column j of
+//      T shared through LDS), giving T_jj = R_jj^-1 and the pivots, while
+//      the other waves finish column block j-1 of T (step 4);
+//   2. row panel R_jk = T_jj^T W_jk (k > j) and U_kj = R_kj T_jj (k < j);
+//   3. trailing update W_kl -= R_jk^T R_jl (j < k <= l);
+//   4. T_ij = -sum_{k=i..j-1} T_ik U_kj (i < j), from T R = I.
+// Tile products run on v_mfma_f64_16x16x4f64, four per 16-deep product:
+// lane (q, li) supplies X[li][4s+q] (A operand) and Y[4s+q][li] (B
+// operand), and holds D[4v+q][li] in component v.  Tiles are stored with
+// element (r, c) at r*16 + (c ^ r), so both operand patterns are free of
+// bank conflicts.  A pivot <= kPivotTol * max diag(G), or a padding column
+// (k >= r), is dependent: its row of R and its row and column of T are zero,
+// which drops that direction exactly as the unblocked recurrence does.
 //   MODE 0: T -> t1; decide whether a second pass is needed (info[0]).
 //   MODE 1: only when info[0]; T of the first pass's P_hat -> tm.
 // -------------------------------------------------------------------------
 constexpr int LC_THREADS = 1024;
+constexpr int LC_WAVES = LC_THREADS / kWave;
+
+__host__ __device__ constexpr int lc_ntiles(int nb) { return nb * (nb + 1) / 2; }
+// index of upper tile (a, b), a <= b, in row-major order of the triangle
+__device__ __forceinline__ int lc_ut(int nb, int a, int b) { return a * nb - a * (a - 1) / 2 + (b - a); }
+__device__ __forceinline__ int lc_sw(int r, int c) { return r * 16 + (c ^ r); }
 
 template <int RP>
 struct LCSmem {
-  double roww[2][RP];
-  double colt[2][RP];
-  double diag[RP];     // diag(G), then sqrt of each pivot (0 when dependent)
+  double W[lc_ntiles(RP / 16)][256];   // G, then R (row panels) and U
+  double T[lc_ntiles(RP / 16)][256];
+  double rowbuf[2][16];
+  double colbuf[2][16];
+  double sdiag[RP];    // sqrt of each pivot (0 when dependent)
   int dep[RP];
   double thr;
 };
 
+// D (+)= sum over 16 of A * B for one tile product; fa(s) / fb(s) give the
+// lane's A / B operand of step s.
+template <class FA, class FB>
+__device__ __forceinline__ d4v lc_mm(FA fa, FB fb, d4v acc) {
+#pragma unroll
+  for (int s = 0; s < 4; ++s) acc = mfma64(fa(s), fb(s), acc);
+  return acc;
+}
+
 template <int RP, int MODE>
 __device__ __forceinline__ void lchol_body(const Desc& d, uint32_t* flags, LCSmem<RP>& sm) {
   if (MODE == 1 && !d.info[0]) return;
-  constexpr int BS = RP / 32;
-  const int t = threadIdx.x, bi = t >> 5, bk = t & 31;
-  const int i0 = BS * bi, k0 = BS * bk;
+  constexpr int NB = RP / 16, NUT = lc_ntiles(NB);
+  const int t = threadIdx.x, wave = t / kWave, lane = t % kWave;
+  const int q = lane >> 4, li = lane & 15;
   const int r = d.r;
-  double W[BS][BS], T[BS][BS];
+  const double* G = d.gsum;
+  // operand readers on swizzled tiles
+  auto rdA = [&](const double* X, int s) { return X[lc_sw(li, 4 * s + q)]; };   // X[li][4s+q]
+  auto rdB = [&](const double* X, int s) { return X[lc_sw(4 * s + q, li)]; };   // X[4s+q][li]
+  auto ldD = [&](const double* X) {
+    d4v v;
 #pragma unroll
-  for (int x = 0; x < BS; ++x)
+    for (int c = 0; c < 4; ++c) v[c] = X[lc_sw(4 * c + q, li)];
+    return v;
+  };
+  auto stD = [&](double* X, d4v v) {
 #pragma unroll
-    for (int y = 0; y < BS; ++y) {
-      W[x][y] = d.gsum[(i0 + x) * RP + k0 + y];
-      T[x][y] = (i0 + x == k0 + y) ? 1.0 : 0.0;
-    }
-  if (bi == bk) {
-#pragma unroll
-    for (int x = 0; x < BS; ++x) sm.diag[i0 + x] = W[x][x];
+    for (int c = 0; c < 4; ++c) X[lc_sw(4 * c + q, li)] = v[c];
+  };
+
+  // G's upper tiles into LDS
+  for (int idx = t; idx < NUT * 256; idx += LC_THREADS) {
+    const int u = idx >> 8, e = idx & 255, rr = e >> 4, cc = e & 15;
+    int a = 0, rem = u;
+    while (rem >= NB - a) { rem -= NB - a; ++a; }
+    sm.W[u][lc_sw(rr, cc)] = G[(16 * a + rr) * RP + 16 * (a + rem) + cc];
   }
-  __syncthreads();
   if (t < kWave) {
     // max of diag(G) over the first wave (max is order-independent)
     double mx = 0.0;
     int nonfinite = 0;
     for (int j = t; j < RP; j += kWave) {
-      const double gv = sm.diag[j];
+      const double gv = G[j * RP + j];
       if (!isfinite(gv)) nonfinite = 1;
       if (gv > mx) mx = gv;
     }
@@ -518,81 +610,138 @@ __device__ __forceinline__ void lchol_body(const Desc& d, uint32_t* flags, LCSme
   __syncthreads();
   const double thr = sm.thr;
 
+  // step 4 for column block jc: wave w (from w0) takes T_ij, i = w - w0
+  auto t_column = [&](int jc, int w0) {
+    const int i = wave - w0;
+    if (i < 0 || i >= jc) return;
+    d4v acc = d4v{0.0, 0.0, 0.0, 0.0};
+    for (int k = i; k < jc; ++k) {
+      const double* Tik = sm.T[lc_ut(NB, i, k)];
+      const double* Ukj = sm.W[lc_ut(NB, k, jc)];
+      acc = lc_mm([&](int s) { return -rdA(Tik, s); }, [&](int s) { return rdB(Ukj, s); }, acc);
+    }
+    stD(sm.T[lc_ut(NB, i, jc)], acc);
+  };
+
 #pragma unroll 1
-  for (int j = 0; j < RP; ++j) {
-    const int buf = j & 1;
-    const int jb = j / BS, jx = j % BS;
-    // (selects instead of W[jx] / T[.][jx]: register arrays need
-    // compile-time indices)
-    if (bi == jb) {
+  for (int j = 0; j < NB; ++j) {
+    if (wave == 0) {
+      // 1. diagonal tile: lane (q, li) holds W_jj[4v+q][li] and T_jj[4v+q][li]
+      double* Wd = sm.W[lc_ut(NB, j, j)];
+      double W[4], T[4];
 #pragma unroll
-      for (int y = 0; y < BS; ++y) {
-        double w = W[0][y];
-#pragma unroll
-        for (int xx = 1; xx < BS; ++xx) w = (jx == xx) ? W[xx][y] : w;
-        sm.roww[buf][k0 + y] = w;
+      for (int v = 0; v < 4; ++v) {
+        W[v] = Wd[lc_sw(4 * v + q, li)];
+        T[v] = (4 * v + q == li) ? 1.0 : 0.0;
       }
-    }
-    if (bk == jb) {
+      double mypiv = 0.0;
+      bool mydep = true;
+#pragma unroll 1
+      for (int jv = 0; jv < 4; ++jv) {
+        // (register arrays need compile-time indices: W[jv] by selects)
 #pragma unroll
-      for (int x = 0; x < BS; ++x) {
-        double v = T[x][0];
+        for (int jq = 0; jq < 4; ++jq) {
+          const int jj = 4 * jv + jq, buf = jq & 1;
+          if (q == jq) {
+            double w = W[0];
 #pragma unroll
-        for (int yy = 1; yy < BS; ++yy) v = (jx == yy) ? T[x][yy] : v;
-        sm.colt[buf][i0 + x] = v;
-      }
-    }
-    __syncthreads();
-    const double piv = sm.roww[buf][j];
-    const bool dep = (j >= r) || (piv <= thr);
-    if (!dep) {
-      const double ip = 1.0 / piv;
-      double ci[BS], cl[BS];
+            for (int v = 1; v < 4; ++v) w = (jv == v) ? W[v] : w;
+            sm.rowbuf[buf][li] = w;   // row jj of W
+          }
+          if (li == jj) {
 #pragma unroll
-      for (int x = 0; x < BS; ++x) {
-        ci[x] = sm.roww[buf][i0 + x] * ip;
-        cl[x] = sm.colt[buf][i0 + x] * ip;
-      }
+            for (int v = 0; v < 4; ++v) sm.colbuf[buf][4 * v + q] = T[v];   // column jj of T
+          }
+          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+          const double piv = sm.rowbuf[buf][jj];
+          const double wk = sm.rowbuf[buf][li];
+          double wi[4], tl[4];
 #pragma unroll
-      for (int y = 0; y < BS; ++y) {
-        const int k = k0 + y;
-        if (k > j) {
-          const double wk = sm.roww[buf][k];
+          for (int v = 0; v < 4; ++v) {
+            wi[v] = sm.rowbuf[buf][4 * v + q];
+            tl[v] = sm.colbuf[buf][4 * v + q];
+          }
+          const bool dep = (16 * j + jj >= r) || (piv <= thr);
+          if (li == jj) {
+            mypiv = piv;
+            mydep = dep;
+          }
+          if (!dep && li > jj) {
+            const double ip = 1.0 / piv;
 #pragma unroll
-          for (int x = 0; x < BS; ++x) {
-            const int i = i0 + x;
-            if (i > j) {
-              if (i <= k) W[x][y] = fma(-ci[x], wk, W[x][y]);
-            } else {
-              T[x][y] = fma(-cl[x], wk, T[x][y]);
+            for (int v = 0; v < 4; ++v) {
+              const int i = 4 * v + q;
+              if (i > jj) {
+                if (i <= li) W[v] = fma(-(wi[v] * ip), wk, W[v]);
+              } else {
+                T[v] = fma(-(tl[v] * ip), wk, T[v]);
+              }
             }
           }
         }
       }
+      const double sq = mydep ? 0.0 : sqrt(mypiv);
+      double* Td = sm.T[lc_ut(NB, j, j)];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) Td[lc_sw(4 * v + q, li)] = (4 * v + q <= li && !mydep) ? T[v] / sq : 0.0;
+      if (q == 0) {
+        sm.sdiag[16 * j + li] = sq;
+        sm.dep[16 * j + li] = mydep ? 1 : 0;
+        if (mydep && 16 * j + li < r && flags) atomicOr(flags, FLAG_RANK_DEFICIENT);
+      }
+    } else if (j > 0) {
+      t_column(j - 1, 1);
     }
-    if (t == 0) {
-      sm.diag[j] = dep ? 0.0 : sqrt(piv);
-      sm.dep[j] = dep ? 1 : 0;
-      if (dep && j < r && flags) atomicOr(flags, FLAG_RANK_DEFICIENT);
+    __syncthreads();
+    // 2. row panel and U, one tile per wave
+    {
+      const double* Tjj = sm.T[lc_ut(NB, j, j)];
+      for (int x = wave; x < NB - 1; x += LC_WAVES) {
+        const int k = x < j ? x : x + 1;
+        if (k > j) {
+          double* Wjk = sm.W[lc_ut(NB, j, k)];
+          const d4v o = lc_mm([&](int s) { return rdB(Tjj, s); }, [&](int s) { return rdB(Wjk, s); },
+                              d4v{0.0, 0.0, 0.0, 0.0});
+          stD(Wjk, o);
+        } else {
+          double* Rkj = sm.W[lc_ut(NB, k, j)];
+          const d4v o = lc_mm([&](int s) { return rdA(Rkj, s); }, [&](int s) { return rdB(Tjj, s); },
+                              d4v{0.0, 0.0, 0.0, 0.0});
+          stD(Rkj, o);
+        }
+      }
+    }
+    __syncthreads();
+    // 3. trailing update over the upper tiles (k, l), j < k <= l
+    if (j + 1 < NB) {
+      const int nr = NB - 1 - j;
+      for (int x = wave; x < nr * (nr + 1) / 2; x += LC_WAVES) {
+        int a = 0, rem = x;
+        while (rem >= nr - a) { rem -= nr - a; ++a; }
+        const int k = j + 1 + a, l = k + rem;
+        const double* Rjk = sm.W[lc_ut(NB, j, k)];
+        const double* Rjl = sm.W[lc_ut(NB, j, l)];
+        double* Wkl = sm.W[lc_ut(NB, k, l)];
+        const d4v o = lc_mm([&](int s) { return -rdB(Rjk, s); }, [&](int s) { return rdB(Rjl, s); }, ldD(Wkl));
+        stD(Wkl, o);
+      }
+      __syncthreads();
     }
   }
+  // 4. for the last column block
+  t_column(NB - 1, 0);
   __syncthreads();
 
   double* out = MODE == 0 ? d.t1 : d.tm;
-#pragma unroll
-  for (int x = 0; x < BS; ++x)
-#pragma unroll
-    for (int y = 0; y < BS; ++y) {
-      const int l = i0 + x, k = k0 + y;
-      double v = 0.0;
-      if (l <= k && !sm.dep[k]) v = T[x][y] / sm.diag[k];
-      out[l * RP + k] = v;
-    }
+  for (int idx = t; idx < RP * RP; idx += LC_THREADS) {
+    const int l = idx / RP, k = idx % RP, a = l >> 4, b = k >> 4;
+    out[idx] = (a <= b) ? sm.T[lc_ut(NB, a, b)][lc_sw(l & 15, k & 15)] : 0.0;
+  }
   if (MODE == 0 && t < kWave) {
     double dmax = 0.0, dmin = 1e308;
     for (int j = t; j < r; j += kWave) {
       if (sm.dep[j]) continue;
-      const double v = sm.diag[j];
+      const double v = sm.sdiag[j];
       dmax = v > dmax ? v : dmax;
       dmin = v < dmin ? v : dmin;
     }
@@ -616,75 +765,117 @@ __global__ __launch_bounds__(LC_THREADS) void k_lchol(OCC_KARGS, uint32_t* flags
 // -------------------------------------------------------------------------
 // k_lapply: P_hat = S T for 128 rows, S = praw, T = t1 (MODE 0) or, in the
 // second pass, S = the first pass's P_hat, T = tm (in place).  fp64
-// arithmetic, fp32 result.  Thread (rb, cb) computes rows 4rb..4rb+3,
-// columns RP/32*cb.. of a 32-row chunk.  The final P_hat (no second pass
-// pending) also goes to the caller's P and, transposed, to phat_t.
+// products on v_mfma_f64_16x16x4f64, fp32 result.  T is upper triangular,
+// so column tile jt of P_hat needs only k < 16 (jt + 1).  The column tiles
+// are paired (jt, NTT-1-jt), which makes every pair the same amount of
+// work; wave w takes pair w % NP and row tiles 2 (w / NP), 2 (w / NP) + 1
+// of each chunk of CR rows, and keeps its two T column tiles in registers
+// for the whole block.  In step s lane (q, li) supplies S[16 rt + li][4 s + q]
+// (A operand, from the staged chunk) and T[4 s + q][16 jt + li] (B operand)
+// and ends with P_hat[16 rt + 4 v + q][16 jt + li] in component v.  The
+// chunk's results are written back into the staging buffer and stored as
+// whole rows to phat and, for the final P_hat (no second pass pending), to
+// the caller's P and transposed to phat_t.
 // -------------------------------------------------------------------------
 template <int RP>
+struct LAShape {
+  static constexpr int NTT = RP / 16, NP = NTT / 2, WPP = 4 / NP, CR = 32 * WPP;
+  static constexpr int LD = RP + 4;
+};
+
+template <int RP>
 struct LASmem {
-  double T[RP * RP];
-  float src[32][RP + 4];
+  float buf[LAShape<RP>::CR][LAShape<RP>::LD];
 };
 
 template <int RP, int MODE>
 __device__ __forceinline__ void la_body(const Desc& d, int b, LASmem<RP>& sm) {
   const uint32_t need = d.info[0];
   if (MODE == 1 && !need) return;
+  using S_ = LAShape<RP>;
+  constexpr int NTT = S_::NTT, NP = S_::NP, CR = S_::CR;
+  static_assert(L_AROWS % CR == 0, "apply chunk must divide the block's rows");
+  constexpr int KA_MAX = 4 * NP;        // steps of the pair's first tile (jt = pair <= NP-1)
+  constexpr int KB_MAX = 4 * NTT;       // steps of the pair's second tile (jt = NTT-1-pair)
   const bool fin = (MODE == 1) || !need;
   const double* Tg = MODE == 0 ? d.t1 : d.tm;
   const float* src = MODE == 0 ? d.praw : d.phat;
-  constexpr int CB = RP / 32;
-  const int t = threadIdx.x, rb = t >> 5, cb = t & 31;
-  for (int idx = t; idx < RP * RP; idx += kBlock) sm.T[idx] = Tg[idx];
+  const int t = threadIdx.x, wave = wave_id(), lane = t & 63;
+  const int q = lane >> 4, li = lane & 15;
+  const int pair = wave % NP, rsub = wave / NP;
+  const int ja = pair, jb = NTT - 1 - pair;
+  const int ka = 4 * (ja + 1), kb = 4 * (jb + 1);   // steps per tile
+  // T column tiles in registers (B operands)
+  double ta[KA_MAX], tb[KB_MAX];
+#pragma unroll
+  for (int s = 0; s < KA_MAX; ++s) ta[s] = (s < ka) ? Tg[(4 * s + q) * RP + 16 * ja + li] : 0.0;
+#pragma unroll
+  for (int s = 0; s < KB_MAX; ++s) tb[s] = (s < kb) ? Tg[(4 * s + q) * RP + 16 * jb + li] : 0.0;
+
   const int r_lo = b * L_AROWS, r_hi = min(d.m, r_lo + L_AROWS);
-  for (int c0 = r_lo; c0 < r_hi; c0 += 32) {
-    for (int idx = t; idx < 32 * RP; idx += kBlock) {
-      const int i = idx / RP, k = idx % RP;
-      sm.src[i][k] = (c0 + i < r_hi) ? src[(int64_t)(c0 + i) * RP + k] : 0.f;
+  for (int c0 = r_lo; c0 < r_hi; c0 += CR) {
+    // stage the chunk's rows of S (rows past m as zeros)
+    for (int idx = t; idx < CR * RP / 4; idx += kBlock) {
+      const int i = idx / (RP / 4), k4 = idx % (RP / 4);
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (c0 + i < r_hi) v = *(const float4*)(src + (int64_t)(c0 + i) * RP + 4 * k4);
+      *(float4*)&sm.buf[i][4 * k4] = v;
     }
     __syncthreads();
-    double acc[4][CB];
+    d4v acc[2][2];
 #pragma unroll
-    for (int x = 0; x < 4; ++x)
-#pragma unroll
-      for (int y = 0; y < CB; ++y) acc[x][y] = 0.0;
-    for (int l = 0; l < RP; ++l) {
-      double sv[4], tv[CB];
-#pragma unroll
-      for (int x = 0; x < 4; ++x) sv[x] = (double)sm.src[4 * rb + x][l];
-#pragma unroll
-      for (int y = 0; y < CB; ++y) tv[y] = sm.T[l * RP + CB * cb + y];
-#pragma unroll
-      for (int x = 0; x < 4; ++x)
-#pragma unroll
-        for (int y = 0; y < CB; ++y) acc[x][y] = fma(sv[x], tv[y], acc[x][y]);
+    for (int u = 0; u < 2; ++u) {
+      acc[u][0] = d4v{0.0, 0.0, 0.0, 0.0};
+      acc[u][1] = d4v{0.0, 0.0, 0.0, 0.0};
     }
-    float o[4][CB];
+    const float* srow0 = sm.buf[32 * rsub + li];
+    const float* srow1 = sm.buf[32 * rsub + 16 + li];
 #pragma unroll
-    for (int x = 0; x < 4; ++x)
+    for (int s = 0; s < KB_MAX; ++s) {
+      if (s < kb) {
+        const double a0 = (double)srow0[4 * s + q], a1 = (double)srow1[4 * s + q];
+        acc[0][1] = mfma64(a0, tb[s], acc[0][1]);
+        acc[1][1] = mfma64(a1, tb[s], acc[1][1]);
+        if (s < KA_MAX && s < ka) {
+          acc[0][0] = mfma64(a0, ta[s], acc[0][0]);
+          acc[1][0] = mfma64(a1, ta[s], acc[1][0]);
+        }
+      }
+    }
+    __syncthreads();
 #pragma unroll
-      for (int y = 0; y < CB; ++y) o[x][y] = (float)acc[x][y];
+    for (int u = 0; u < 2; ++u)
 #pragma unroll
-    for (int x = 0; x < 4; ++x) {
-      const int row = c0 + 4 * rb + x;
+      for (int v = 0; v < 4; ++v) {
+        float* orow = sm.buf[16 * (2 * rsub + u) + 4 * v + q];
+        orow[16 * ja + li] = (float)acc[u][0][v];
+        orow[16 * jb + li] = (float)acc[u][1][v];
+      }
+    __syncthreads();
+    // whole rows out
+    for (int idx = t; idx < CR * RP / 4; idx += kBlock) {
+      const int i = idx / (RP / 4), k4 = idx % (RP / 4);
+      const int row = c0 + i;
       if (row < r_hi) {
-        st_f<CB>(d.phat + (int64_t)row * RP + CB * cb, o[x]);
+        const float4 v = *(const float4*)&sm.buf[i][4 * k4];
+        *(float4*)(d.phat + (int64_t)row * RP + 4 * k4) = v;
         if (fin) {
+          const float vv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-          for (int y = 0; y < CB; ++y) {
-            const int k = CB * cb + y;
-            if (k < d.r) d.P[(int64_t)row * d.r + k] = o[x][y];
-          }
+          for (int e = 0; e < 4; ++e)
+            if (4 * k4 + e < d.r) d.P[(int64_t)row * d.r + 4 * k4 + e] = vv[e];
         }
       }
     }
     if (fin) {
-      // rows past m carry zeros (their source rows were staged as 0)
-#pragma unroll
-      for (int y = 0; y < CB; ++y) {
-        const int k = CB * cb + y;
-        *(float4*)(d.phat_t + (int64_t)k * d.m_pad + c0 + 4 * rb) =
-            make_float4(o[0][y], o[1][y], o[2][y], o[3][y]);
+      // transposed: rank k, four consecutive rows per thread (rows past m
+      // carry zeros, their source rows were staged as 0)
+      for (int idx = t; idx < RP * CR / 4; idx += kBlock) {
+        const int k = idx / (CR / 4), i4 = idx % (CR / 4);
+        if (c0 + 4 * i4 < d.m_pad)
+          *(float4*)(d.phat_t + (int64_t)k * d.m_pad + c0 + 4 * i4) =
+              make_float4(sm.buf[4 * i4][k], sm.buf[4 * i4 + 1][k], sm.buf[4 * i4 + 2][k],
+                          sm.buf[4 * i4 + 3][k]);
       }
     }
     __syncthreads();

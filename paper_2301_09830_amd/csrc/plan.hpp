@@ -169,7 +169,7 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0) {
   t.blocks[K_QPAD] = cdiv(t.n_pad, 8);    // 8-column tiles (k_qpadl)
   t.blocks[K_PASS_P] = row_tiles * t.sp;
   t.blocks[K_PGRAM] = t.ng;
-  t.blocks[K_GSUM] = cdiv((int64_t)rp * rp, kBlock);
+  t.blocks[K_GSUM] = cdiv((int64_t)rp * rp, kBlock / 8);   // 32 entries per block
   t.blocks[K_GRAM2] = t.ng;
   t.blocks[K_APPLY] = cdiv(m, L_AROWS);
   t.blocks[K_PASS_Q] = ctq * t.sq;
