@@ -35,6 +35,7 @@ sys.path.insert(0, ROOT)
 METRIC = "compress+decompress+err-update input GB/s and % of HBM roofline, 1 MI355X"
 HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3     # dense fp32 matrix-core peak of the MI355X
+BF16_MFMA_PEAK_TFLOPS = 2500.0    # dense bf16 matrix-core peak of the MI355X
 PROFILES = os.path.join(ROOT, "profiles")
 CSRC = os.path.join(ROOT, "paper_2301_09830_amd", "csrc")
 
@@ -64,6 +65,19 @@ def kernel_alg_bytes(kernel: str, elements: int, m_bytes: int) -> int | None:
            "err_only": m_bytes + 8, "pass_p_first": m_bytes + 8, "pass_p_a": 4,
            "pass_q_a": 4, "mhat_err_a": 12, "err_only_a": 8}.get(kernel)
     return None if per is None else per * elements
+
+
+def product_engine(kernel: str, m_dtype: str, rank: int) -> tuple:
+    """(matrix-core peak in TFLOP/s of ALGORITHMIC flops, engine) of a product kernel.
+
+    Ranks padded to <= 16 and fp32 inputs run fp32 products on fp32 matrix
+    cores.  For bf16 M at padded ranks 32..128 the left and right products
+    run on bf16 matrix cores with split operands, three bf16 products per
+    algorithmic product, so the algorithmic flops have a third of the bf16
+    peak; the reconstruction stays on fp32 matrix cores."""
+    if m_dtype == "bf16" and rank > 16 and kernel.startswith("pass_"):
+        return BF16_MFMA_PEAK_TFLOPS / 3.0, "bf16 matrix cores, split operands (3 products)"
+    return FP32_MFMA_PEAK_TFLOPS, "fp32 matrix cores"
 
 
 def kernel_alg_flops(kernel: str, elements: int, rank: int) -> int | None:
@@ -366,17 +380,19 @@ def main() -> int:
             flops = kernel_alg_flops(dom, elements, w.rank)
             traffic = load_traffic(dom, w.name, elements)
             # the bound is whichever resource the kernel's algorithmic work
-            # needs longer on: HBM bytes at 8 TB/s or fp32 MFMA flops
-            mfma_bound = flops is not None and flops / FP32_MFMA_PEAK_TFLOPS > per_launch / HBM_PEAK_GBS * 1e3
+            # needs longer on: HBM bytes at 8 TB/s or its flops on the matrix
+            # cores it runs on
+            mfma_peak, engine = product_engine(dom, w.m_dtype, w.rank)
+            mfma_bound = flops is not None and flops / mfma_peak > per_launch / HBM_PEAK_GBS * 1e3
             if mfma_bound:
-                achieved, peak, unit = flops / avg_s / 1e12, FP32_MFMA_PEAK_TFLOPS, "TFLOP/s"
+                achieved, peak, unit = flops / avg_s / 1e12, round(mfma_peak, 1), "TFLOP/s"
             else:
                 achieved, peak, unit = per_launch / avg_s / 1e9, HBM_PEAK_GBS, "GB/s"
             roofline = {"kernel": dom, "bound": "mfma" if mfma_bound else "hbm",
                         "achieved": round(achieved, 1), "peak": peak, "unit": unit,
                         "frac": round(achieved / peak, 4),
                         "traffic": traffic, "alg_bytes_per_launch": int(per_launch),
-                        "alg_flops_per_launch": flops,
+                        "alg_flops_per_launch": flops, "engine": engine,
                         "hbm_achieved_gbs": round(per_launch / avg_s / 1e9, 1),
                         "avg_launch_us": round(avg_s * 1e6, 3)}
 

@@ -8,6 +8,9 @@
 #include <algorithm>
 #include <cstdio>
 #include <cstring>
+#include <map>
+#include <mutex>
+#include <tuple>
 #include <type_traits>
 #include <vector>
 
@@ -152,6 +155,68 @@ struct Batch {
   size_t ws_needed = 0;
 };
 
+// ----------------------------------------------------------------------------
+// resident blocks of the large-rank streaming kernels
+// ----------------------------------------------------------------------------
+// From the HIP occupancy calculator for the kernel instances of a fused step
+// on the current device.  When no device answers (a host without a GPU) the
+// defaults of Slots apply, so workspace sizes stay computable there; a
+// workspace sized on one device type may be too small on another, which the
+// call reports as OCC_E_WORKSPACE.
+template <int DT, int RP>
+Slots device_slots_for(int dev) {
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus < 1) {
+    (void)hipGetLastError();
+    return Slots{};
+  }
+  constexpr bool X3 = DT == DT_BF16;
+  int bp = 0, bq = 0, bm = 0;
+  bool ok = hipOccupancyMaxActiveBlocksPerMultiprocessor(&bp, k_lp<DT, RP, SA_MERR_SAVE, X3>,
+                                                         kBlock, 0) == hipSuccess;
+  if constexpr (X3)
+    ok = ok && hipOccupancyMaxActiveBlocksPerMultiprocessor(&bq, k_lqx<DT_F32, RP, SA_SAVED>,
+                                                            kBlock, 0) == hipSuccess;
+  else
+    ok = ok && hipOccupancyMaxActiveBlocksPerMultiprocessor(&bq, k_lq<DT_F32, RP, SA_SAVED>,
+                                                            kBlock, 0) == hipSuccess;
+  ok = ok && hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                 &bm, k_ml<DT_F32, RP, SA_SAVED, 0, true, true>, kBlock, 0) == hipSuccess;
+  if (!ok || bp < 1 || bq < 1 || bm < 1) {
+    (void)hipGetLastError();
+    return Slots{};
+  }
+  Slots sl;
+  sl.p = (int64_t)cus * bp;
+  sl.q = (int64_t)cus * bq;
+  sl.m = (int64_t)cus * bm;
+  return sl;
+}
+
+Slots device_slots(int dt, int rp) {
+  if (rp <= kFusedMaxRank) return Slots{};
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) {
+    (void)hipGetLastError();
+    return Slots{};
+  }
+  static std::mutex mu;
+  static std::map<std::tuple<int, int, int>, Slots> cache;
+  std::lock_guard<std::mutex> lock(mu);
+  const auto key = std::make_tuple(dev, dt, rp);
+  const auto it = cache.find(key);
+  if (it != cache.end()) return it->second;
+  Slots sl;
+  with_rp(rp, [&](auto RPc) {
+    constexpr int RP = decltype(RPc)::value;
+    if constexpr (RP > kFusedMaxRank)
+      sl = dt == DT_F32 ? device_slots_for<DT_F32, RP>(dev) : device_slots_for<DT_BF16, RP>(dev);
+  });
+  cache[key] = sl;
+  return sl;
+}
+
 size_t table_bytes(int count) { return count > 1 ? align_up((size_t)count * sizeof(Desc)) : 0; }
 
 // Turn the workspace offsets stored in the descriptors into device addresses.
@@ -200,11 +265,13 @@ occ_status_t plan_batch(const occ_mat_t* mats, int count, int rank, int iters, u
   size_t off = kHeaderBytes + table_bytes(count);
   double total_elems = 0.0;
   for (int j = 0; j < count; ++j) total_elems += (double)mats[j].rows * (double)mats[j].cols;
+  const Slots slots = device_slots(dt, b.rp);
   b.descs.assign(count, Desc{});
   for (int k = 0; k < K_NUM; ++k) b.blocks[k] = 0;
   for (int j = 0; j < count; ++j) {
     const occ_mat_t& a = mats[j];
-    const Tiling t = make_tiling(a.rows, a.cols, b.rp, (double)a.rows * (double)a.cols / total_elems);
+    const Tiling t =
+        make_tiling(a.rows, a.cols, b.rp, (double)a.rows * (double)a.cols / total_elems, slots);
     const Regions g = matrix_regions(a.rows, a.cols, b.rp, t);
     Desc& d = b.descs[j];
     d.m = (int32_t)a.rows;

@@ -202,7 +202,7 @@ __device__ __forceinline__ void pm_body(const Desc& d, int b, PMSmem& sm) {
     sm.rows[i * RP + k] = (i < nr) ? (double)s : 0.0;
   }
   __syncthreads();
-  gram_rows_store<RP, PM_THREADS>(sm.rows, nr, d.gpart + (int64_t)b * RP * RP);
+  gram_rows_store<RP, PM_THREADS>(sm.rows, nr, d.gpart + (int64_t)b * (RP * (RP + 1) / 2));
 }
 
 template <int DT, bool VEC, int RP>

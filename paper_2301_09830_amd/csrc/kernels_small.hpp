@@ -9,10 +9,10 @@
 //            each block owns whole rows, so it stores final rows of P and
 //            their fp64 Gram partial.
 //   k_orth16 every block sums the Gram partials and runs the Cholesky
-//            factorisation (CholeskyQR first pass; the second pass only when
-//            the first found the Gram badly conditioned) -- the same
-//            deterministic computation in each block, so no hand-off is
-//            needed -- then forms P_hat = P T for its own 128 rows.
+//            factorisation G = R^T R (CholeskyQR first pass; the second pass
+//            only when the first found the Gram badly conditioned) -- the
+//            same deterministic computation in each block, so no hand-off is
+//            needed -- then forms P_hat = P R^-1 for its own 128 rows.
 //   k_qm     right product partials A^T P_hat over row splits (matrix cores).
 //   k_qred16 Q = sum of the row-split partials.
 // and after the last round
@@ -80,44 +80,37 @@ __device__ __forceinline__ const float* q_src(const Desc& d) { return d.r == RP 
 template <int RP>
 __device__ __forceinline__ const float* p_src(const Desc& d) { return d.r == RP ? d.P : d.phat; }
 
-// dst[e] = sum_{g < parts} src[g][e] for e < RP*RP (fixed order); loads are
-// issued in batches of 16 so a thread waits for memory once per batch.
+// Packed upper triangle of an RP x RP symmetric matrix: entry p < NP
+// (NP = RP (RP + 1) / 2) is (k, l) with k <= l, row by row.
 template <int RP>
-__device__ __forceinline__ void sum_partials(const double* src, int parts, double* dst) {
-  for (int e = threadIdx.x; e < RP * RP; e += kBlock) {
-    double s = 0.0;
-    for (int g0 = 0; g0 < parts; g0 += 16) {
-      double v[16];
-#pragma unroll
-      for (int u = 0; u < 16; ++u)
-        v[u] = (g0 + u < parts) ? src[(int64_t)(g0 + u) * RP * RP + e] : 0.0;
-#pragma unroll
-      for (int u = 0; u < 16; ++u)
-        if (g0 + u < parts) s = (g0 + u == 0) ? v[u] : s + v[u];
-    }
-    dst[e] = s;
-  }
+__device__ __forceinline__ void upper_entry(int p, int& k, int& l) {
+  int kk = 0, rem = p;
+  while (rem >= RP - kk) { rem -= RP - kk; ++kk; }
+  k = kk;
+  l = kk + rem;
 }
 
-
-// Gram of `nr` rows held in LDS as doubles (row pitch RP), full matrix.
+// Gram of `nr` rows held in LDS as doubles (row pitch RP): the packed upper
+// triangle, written to dst[0 .. NP).
 template <int RP, int NT = kBlock>
 __device__ __forceinline__ void gram_rows_store(const double* rows, int nr, double* dst) {
-  for (int e = threadIdx.x; e < RP * RP; e += NT) {
-    const int k = e / RP, l = e % RP;
+  constexpr int NP = RP * (RP + 1) / 2;
+  for (int p = threadIdx.x; p < NP; p += NT) {
+    int k, l;
+    upper_entry<RP>(p, k, l);
     double s = 0.0;
     for (int i = 0; i < nr; ++i) s = fma(rows[i * RP + k], rows[i * RP + l], s);
-    dst[e] = s;
+    dst[p] = s;
   }
 }
 
 // -------------------------------------------------------------------------
-// k_orth16: Gram = sum of the row-block partials, Cholesky, T = L^-T
+// k_orth16: Gram = sum of the row-block partials, Cholesky G = R^T R
 // (CholeskyQR first pass) and, only when the first pass lost orthogonality,
-// the second pass; then P_hat = P T.  Blocks of 1024 threads: thread
-// (pair, group) sums a slice of the upper-triangle partials with all its
-// loads in flight, the slices are added in LDS in order, and wave 0
-// factorises with the matrix in registers.
+// the second pass; then P_hat = P R^-1 by forward substitution, one row per
+// thread.  Blocks of 1024 threads: thread (pair, group) sums a slice of the
+// packed partials with all its loads in flight, the slices are added in LDS
+// in order, and wave 0 factorises with one matrix entry per lane slot.
 // -------------------------------------------------------------------------
 constexpr int CH_THREADS = 1024;
 static_assert(F_ORTHROWS <= CH_THREADS, "k_orth16 forms one P_hat row per thread");
@@ -127,23 +120,11 @@ constexpr int CH_BATCH = 20;      // partial loads in flight per thread
 struct CholSmem {
   double part[8][16 * 17 / 2];
   double G[16 * 16];
-  double T1[16 * 16];
+  double R[2][16 * 16];       // factors of the two passes (upper triangle, row-major)
+  double inv[2][16];          // 1 / R[k][k], zero for a dependent column
+  double rowbuf[2][16];       // pivot row of the current Schur complement
   double rows[CH_CHUNK * 16];
   uint32_t need;
-};
-
-__device__ __forceinline__ double readlane_d(double v, int lane) {
-  const unsigned long long u = (unsigned long long)__double_as_longlong(v);
-  const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)u, lane);
-  const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(u >> 32), lane);
-  return __longlong_as_double((long long)(((unsigned long long)hi << 32) | lo));
-}
-
-template <int RP>
-struct CholOut {
-  double x[RP];       // lane c: column c of X = L^-1 (dependent rows zero)
-  uint32_t defmask;   // dependent columns
-  double pmax, pmin;  // extreme pivots (squared diagonal of L) over independent columns < r
 };
 
 // 1/sqrt(v) for v > 0: hardware estimate refined by two Newton steps
@@ -156,77 +137,120 @@ __device__ __forceinline__ double rsqrt_nr(double v) {
   return fma(0.5 * y, e, y);
 }
 
-// Cholesky G = L L^T of the leading RP x RP block of G (rows/columns >= r
-// are padding and count as dependent).  A pivot <= kPivotTol * max diag(G)
-// marks its column dependent: the column of L is zero below a unit
-// diagonal and later columns ignore it.  Executed by one wave with the
-// matrix in registers: lane i holds row i, and values of other rows are
-// broadcast with v_readlane (compile-time indices), so the sequential
-// factorisation has no memory latency.  Only reciprocals of the diagonal
-// are formed (one refined rsqrt per pivot; no divides).
+// LDS writes of this wave are complete before its next LDS read is issued
+// (LDS executes one wave's instructions in order; this keeps the compiler
+// from moving the reads above the writes and waits for the writes).
+__device__ __forceinline__ void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+struct CholInfo {
+  uint32_t defmask;   // dependent columns
+  double pmax, pmin;  // extreme pivots (squared diagonal of R) over independent columns
+};
+
+// Cholesky G = R^T R of the leading RP x RP block of the symmetric G (LDS,
+// row-major), by one wave; R (upper triangle, zero below) and the inverse
+// diagonal go to LDS.  Right-looking on the upper triangle: lane slot
+// (lane, q) owns entry e = lane + 64 q = (i, j) of the Schur complement; at
+// step k the owners of row k publish it, every slot reads the pivot and its
+// two row-k factors, and entries with k < i <= j are updated.  Columns >= r
+// are padding; a pivot <= kPivotTol * max diag(G) marks its column
+// dependent: that row of R is the unit row, its inverse diagonal is zero (the
+// column of P_hat is zero) and later steps ignore it.  NaN pivots are not
+// dependent: they propagate like the data.
 template <int RP>
-__device__ __forceinline__ CholOut<RP> chol_regs(const double* G, int r, uint32_t* flags) {
+__device__ __forceinline__ CholInfo chol_lanes(const double* G, int r, double* R, double* inv,
+                                              double (*rowbuf)[16], uint32_t* flags) {
+  constexpr int NE = (RP * RP + kWave - 1) / kWave;
   const int lane = threadIdx.x & 63;
-  CholOut<RP> o;
-  double a[RP];
+  double w[NE];
+  int ei[NE], ej[NE];
+  bool up[NE];
 #pragma unroll
-  for (int k = 0; k < RP; ++k) a[k] = (lane < RP) ? G[lane * RP + k] : 0.0;
+  for (int q = 0; q < NE; ++q) {
+    const int e = lane + kWave * q;
+    ei[q] = e / RP;
+    ej[q] = e % RP;
+    up[q] = e < RP * RP && ei[q] <= ej[q];
+    w[q] = up[q] ? G[e] : 0.0;
+  }
   double maxdiag = 0.0;
   bool nonfinite = false;
 #pragma unroll
-  for (int j = 0; j < RP; ++j) {
-    const double gjj = readlane_d(a[j], j);
-    nonfinite = nonfinite || !isfinite(gjj);
-    maxdiag = gjj > maxdiag ? gjj : maxdiag;
+  for (int k = 0; k < RP; ++k) {
+    const double gkk = G[k * RP + k];
+    nonfinite = nonfinite || !isfinite(gkk);
+    maxdiag = gkk > maxdiag ? gkk : maxdiag;
   }
-  if (lane == 0 && nonfinite && flags) atomicOr(flags, FLAG_NONFINITE);
   const double thr = kPivotTol * maxdiag;
-  uint32_t defmask = 0;
-  bool any_dep = false;
-  double invd[RP];
+  CholInfo o;
+  o.defmask = 0;
   o.pmax = 0.0;
   o.pmin = 1e308;
 #pragma unroll
-  for (int j = 0; j < RP; ++j) {
-    const double piv = readlane_d(a[j], j);
-    const bool dep = (j >= r) || (piv <= thr);
-    any_dep = any_dep || (dep && j < r);
-    defmask |= dep ? (1u << j) : 0u;
+  for (int k = 0; k < RP; ++k) {
+    double* rb = rowbuf[k & 1];
+#pragma unroll
+    for (int q = 0; q < NE; ++q)
+      if (up[q] && ei[q] == k) rb[ej[q]] = w[q];
+    wave_lds_sync();
+    const double piv = rb[k];
+    double ri[NE], rj[NE];
+#pragma unroll
+    for (int q = 0; q < NE; ++q) {
+      ri[q] = rb[ei[q] < RP ? ei[q] : 0];
+      rj[q] = rb[ej[q]];
+    }
+    const bool dep = (k >= r) || (piv <= thr);
+    o.defmask |= dep ? (1u << k) : 0u;
     if (!dep) {
       o.pmax = piv > o.pmax ? piv : o.pmax;
       o.pmin = piv < o.pmin ? piv : o.pmin;
     }
-    // NaN pivots are not "dependent": they propagate into T like the data
-    const double inv = dep ? 1.0 : rsqrt_nr(piv);
-    invd[j] = inv;
-    if (lane == j) a[j] = dep ? 1.0 : piv * inv;
-    else if (lane > j) a[j] = dep ? 0.0 : a[j] * inv;
+    const double ik = dep ? 0.0 : rsqrt_nr(piv);
+    if (lane == 0) inv[k] = ik;
 #pragma unroll
-    for (int k = j + 1; k < RP; ++k) {
-      const double lkj = readlane_d(a[j], k);
-      if (lane >= k) a[k] -= a[j] * lkj;
+    for (int q = 0; q < NE; ++q) {
+      if (up[q] && ei[q] == k)
+        R[k * RP + ej[q]] = (ej[q] == k) ? (dep ? 1.0 : piv * ik) : (dep ? 0.0 : w[q] * ik);
+      if (!dep && up[q] && ei[q] > k) w[q] = fma(-(ri[q] * ik), rj[q] * ik, w[q]);
     }
   }
-  if (lane == 0 && any_dep && flags) atomicOr(flags, FLAG_RANK_DEFICIENT);
 #pragma unroll
-  for (int i = 0; i < RP; ++i) {
-    double s = (lane == i) ? 1.0 : 0.0;
-#pragma unroll
-    for (int k = 0; k < i; ++k) s -= readlane_d(a[k], i) * o.x[k];
-    o.x[i] = (i >= lane && !((defmask >> i) & 1u)) ? s * invd[i] : 0.0;
+  for (int q = 0; q < NE; ++q) {
+    const int e = lane + kWave * q;
+    if (e < RP * RP && ei[q] > ej[q]) R[e] = 0.0;
   }
-  o.defmask = defmask;
+  const uint32_t live = r >= 32 ? 0xffffffffu : ((1u << r) - 1u);
+  if (lane == 0 && flags) {
+    if (nonfinite) atomicOr(flags, FLAG_NONFINITE);
+    if (o.defmask & live) atomicOr(flags, FLAG_RANK_DEFICIENT);
+  }
   return o;
 }
 
-// The first pass lost orthogonality when diag(L) spans more than
+// The first pass lost orthogonality when diag(R) spans more than
 // kSecondPassCond, i.e. the pivots span more than its square.
-template <int RP>
-__device__ __forceinline__ uint32_t needs_second_pass(const CholOut<RP>& o) {
+__device__ __forceinline__ uint32_t needs_second_pass(const CholInfo& o) {
   return (o.pmax > 0.0 && o.pmax > kSecondPassCond * kSecondPassCond * o.pmin) ? 1u : 0u;
 }
 
-// Gram (upper triangle, fp64) of `nsrc` stacked RP x RP partials, by all
+// x <- x R^-1 for one row (forward substitution, fp64), R upper triangular
+// with inverse diagonal inv (zero for a dependent column, which zeroes it).
+template <int RP>
+__device__ __forceinline__ void solve_row(double* x, const double* R, const double* inv) {
+#pragma unroll
+  for (int j = 0; j < RP; ++j) {
+    // one column of R in flight at a time: hoisting all of its LDS reads out
+    // of the loop would take about 270 VGPRs
+    asm volatile("" ::: "memory");
+    double v = x[j];
+#pragma unroll
+    for (int k = 0; k < j; ++k) v = fma(-x[k], R[k * RP + j], v);
+    x[j] = v * inv[j];
+  }
+}
+
+// Gram (upper triangle, fp64) of `nsrc` stacked packed partials, by all
 // CH_THREADS threads; result (full symmetric) in G.
 template <int RP>
 __device__ __forceinline__ void gram_sum_all(const double* src, int nsrc, CholSmem& sm, double* G) {
@@ -235,16 +259,13 @@ __device__ __forceinline__ void gram_sum_all(const double* src, int nsrc, CholSm
   const int t = threadIdx.x;
   const int p = t % NP, q = t / NP;
   if (q < NG) {
-    int k = 0, rem = p;
-    while (rem >= RP - k) { rem -= RP - k; ++k; }
-    const int e = k * RP + (k + rem);
     const int per = (nsrc + NG - 1) / NG;
     const int g0 = min(nsrc, q * per), g1 = min(nsrc, g0 + per);
     double s = 0.0;
     for (int gb = g0; gb < g1; gb += CH_BATCH) {
       double v[CH_BATCH];
 #pragma unroll
-      for (int u = 0; u < CH_BATCH; ++u) v[u] = (gb + u < g1) ? src[(int64_t)(gb + u) * RP * RP + e] : 0.0;
+      for (int u = 0; u < CH_BATCH; ++u) v[u] = (gb + u < g1) ? src[(int64_t)(gb + u) * NP + p] : 0.0;
 #pragma unroll
       for (int u = 0; u < CH_BATCH; ++u)
         if (gb + u < g1) s = (gb + u == g0) ? v[u] : s + v[u];
@@ -255,83 +276,51 @@ __device__ __forceinline__ void gram_sum_all(const double* src, int nsrc, CholSm
   if (t < NP) {
     double s = sm.part[0][t];
     for (int qq = 1; qq < NG; ++qq) s += sm.part[qq][t];
-    int k = 0, rem = t;
-    while (rem >= RP - k) { rem -= RP - k; ++k; }
-    const int l = k + rem;
+    int k, l;
+    upper_entry<RP>(t, k, l);
     G[k * RP + l] = s;
     G[l * RP + k] = s;
   }
   __syncthreads();
 }
 
-// P_hat row = P row * T (fp64), written to the caller's P and the padded
-// copy.
+// Row of P (fp64) from the unorthogonalised P.
 template <int RP>
-__device__ __forceinline__ void phat_row(const Desc& d, int64_t row, const double* T) {
-  // keep the T reads here: hoisting all of them out of a row loop costs ~270 VGPRs
-  asm volatile("" ::: "memory");
-  float p[RP];
+__device__ __forceinline__ void p_row(const Desc& d, int64_t row, double* x) {
 #pragma unroll
   for (int k = 0; k < RP; k += 4) {
     const float4 v = *(const float4*)(d.praw + row * RP + k);
-    p[k] = v.x; p[k + 1] = v.y; p[k + 2] = v.z; p[k + 3] = v.w;
+    x[k] = v.x; x[k + 1] = v.y; x[k + 2] = v.z; x[k + 3] = v.w;
   }
-  float out[RP];
-#pragma unroll
-  for (int k = 0; k < RP; ++k) {
-    asm volatile("" ::: "memory");   // one column of T in flight at a time
-    double v = 0.0;
-#pragma unroll
-    for (int l = 0; l <= k; ++l) v = fma((double)p[l], T[l * RP + k], v);
-    out[k] = (float)v;
-  }
-  // the padded copy is always written: the reconstruction pass reads it with
-  // 16-byte loads (the caller's P has no alignment guarantee)
-#pragma unroll
-  for (int k = 0; k < RP; k += 4)
-    *(float4*)(d.phat + row * RP + k) = make_float4(out[k], out[k + 1], out[k + 2], out[k + 3]);
-#pragma unroll
-  for (int k = 0; k < RP; ++k)
-    if (k < d.r) d.P[row * d.r + k] = out[k];
 }
 
 // k_orth16 block b: full Gram, Cholesky (and the second pass when needed),
 // computed identically in every block, then P_hat for rows
-// [b * F_ORTHROWS, (b + 1) * F_ORTHROWS).  Block 0 also stores T1, Tm, the
-// second-pass decision and the numeric flags.
+// [b * F_ORTHROWS, (b + 1) * F_ORTHROWS), written to the caller's P and the
+// padded copy.  Block 0 also stores the second-pass decision and the
+// numeric flags.
 template <int RP>
 __device__ __forceinline__ void orth16_body(const Desc& d, int b, uint32_t* flags, CholSmem& sm) {
   const int t = threadIdx.x;
   uint32_t* fl = (b == 0) ? flags : nullptr;
   gram_sum_all<RP>(d.gpart, d.ng, sm, sm.G);
   if (t < kWave) {
-    const CholOut<RP> o = chol_regs<RP>(sm.G, d.r, fl);
-    const uint32_t need = needs_second_pass<RP>(o);
-    if (t < RP) {
-#pragma unroll
-      for (int i = 0; i < RP; ++i) {
-        sm.T1[t * RP + i] = o.x[i];
-        if (b == 0) {
-          d.t1[t * RP + i] = o.x[i];
-          if (!need) d.tm[t * RP + i] = o.x[i];
-        }
-      }
-    }
+    const CholInfo o = chol_lanes<RP>(sm.G, d.r, sm.R[0], sm.inv[0], sm.rowbuf, fl);
+    const uint32_t need = needs_second_pass(o);
     if (t == 0) {
       if (b == 0) d.info[0] = need;
       sm.need = need;
     }
   }
   __syncthreads();
-  const double* T = sm.T1;
-  if (sm.need) {
-    // Second pass: Gram of P_hat1 = P T1 (fp64) over all rows, in chunks.
+  const uint32_t need = sm.need;
+  if (need) {
+    // Second pass: Gram of P_hat1 = P R1^-1 (fp64) over all rows, in chunks.
     constexpr int NP = RP * (RP + 1) / 2;
     constexpr int NG = CH_THREADS / NP < 8 ? CH_THREADS / NP : 8;
     const int p = t % NP, q = t / NP;
-    int pk_ = 0, rem = p;
-    while (rem >= RP - pk_) { rem -= RP - pk_; ++pk_; }
-    const int pl_ = pk_ + rem;
+    int pk_, pl_;
+    upper_entry<RP>(p, pk_, pl_);
     double acc = 0.0;
     const int per = (CH_CHUNK + NG - 1) / NG;
     for (int c0 = 0; c0 < d.m; c0 += CH_CHUNK) {
@@ -341,15 +330,8 @@ __device__ __forceinline__ void orth16_body(const Desc& d, int b, uint32_t* flag
 #pragma unroll
         for (int k = 0; k < RP; ++k) v[k] = 0.0;
         if (row < d.m) {
-          asm volatile("" ::: "memory");
-#pragma unroll
-          for (int k = 0; k < RP; ++k) {
-            double sacc = 0.0;
-#pragma unroll
-            for (int l = 0; l <= k; ++l)
-              sacc = fma((double)d.praw[(int64_t)row * RP + l], sm.T1[l * RP + k], sacc);
-            v[k] = sacc;
-          }
+          p_row<RP>(d, row, v);
+          solve_row<RP>(v, sm.R[0], sm.inv[0]);
         }
 #pragma unroll
         for (int k = 0; k < RP; ++k) sm.rows[t * RP + k] = v[k];
@@ -370,30 +352,27 @@ __device__ __forceinline__ void orth16_body(const Desc& d, int b, uint32_t* flag
       sm.G[pl_ * RP + pk_] = sacc;
     }
     __syncthreads();
-    if (t < kWave) {
-      const CholOut<RP> o2 = chol_regs<RP>(sm.G, d.r, fl);
-      // Tm = T1 T2 with T2 = X2^T: Tm[l][k] = sum_{l <= p <= k} T1[l][p] X2[k][p];
-      // lane p holds X2[k][p] in o2.x[k].  G is no longer read (chol_regs
-      // loaded it into registers first), so Tm overwrites it row by row.
-#pragma unroll
-      for (int k = 0; k < RP; ++k) {
-        double sacc = 0.0;
-#pragma unroll
-        for (int pp = 0; pp < RP; ++pp) {
-          const double x2 = readlane_d(o2.x[k], pp);
-          if (t < RP && pp >= t && pp <= k) sacc = fma(sm.T1[t * RP + pp], x2, sacc);
-        }
-        if (t < RP) {
-          sm.G[t * RP + k] = sacc;
-          if (b == 0) d.tm[t * RP + k] = sacc;
-        }
-      }
-    }
+    if (t < kWave) chol_lanes<RP>(sm.G, d.r, sm.R[1], sm.inv[1], sm.rowbuf, fl);
     __syncthreads();
-    T = sm.G;
   }
   const int64_t row = (int64_t)b * F_ORTHROWS + t;
-  if (t < F_ORTHROWS && row < d.m) phat_row<RP>(d, row, T);
+  if (t < F_ORTHROWS && row < d.m) {
+    double x[RP];
+    p_row<RP>(d, row, x);
+    solve_row<RP>(x, sm.R[0], sm.inv[0]);
+    if (need) solve_row<RP>(x, sm.R[1], sm.inv[1]);
+    float out[RP];
+#pragma unroll
+    for (int k = 0; k < RP; ++k) out[k] = (float)x[k];
+    // the padded copy is always written: the reconstruction pass reads it
+    // with 16-byte loads (the caller's P has no alignment guarantee)
+#pragma unroll
+    for (int k = 0; k < RP; k += 4)
+      *(float4*)(d.phat + row * RP + k) = make_float4(out[k], out[k + 1], out[k + 2], out[k + 3]);
+#pragma unroll
+    for (int k = 0; k < RP; ++k)
+      if (k < d.r) d.P[row * d.r + k] = out[k];
+  }
 }
 
 template <int RP>

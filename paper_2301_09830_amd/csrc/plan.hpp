@@ -103,7 +103,6 @@ constexpr int L_GROWS = 256;      // Gram partials: rows per block
 constexpr int L_AROWS = 128;      // P_hat = P T: rows per block
 constexpr int L_QG = 8;           // right product: rows per LDS stage
 constexpr int64_t L_SPLIT_BLOCKS = 1024;  // split products: blocks over the whole batch
-constexpr int64_t L_MIN_BLOCKS = 256;     // ... and at least this many per matrix
 constexpr int64_t L_MIN_COLS = 1024;      // left product: columns per split, at least
 constexpr int64_t L_MIN_ROWS = 1024;      // right product: rows per split, at least
 constexpr int64_t L_MIN_SPLIT = 512;      // columns / rows per split, at least
@@ -114,9 +113,24 @@ __host__ __device__ constexpr int lq_block_cols(int rp) { return 128 * lq_cpl(rp
 __host__ __device__ constexpr int lm_tiles(int rp) { return rp >= 64 ? 1 : 2; }
 __host__ __device__ constexpr int lm_block_cols(int rp) { return 128 * lm_tiles(rp); }
 
+// Blocks of each large-rank streaming kernel that are resident on the
+// device at once (compute units x blocks per compute unit).  Grids are
+// sized in whole multiples of these: blocks of a pass do equal work, so a
+// grid of 1.33 rounds takes as long as 2.
+struct Slots {
+  int64_t p = 1024, q = 1024, m = 1024;   // left product, right product, reconstruction
+};
+
+// The multiple of `slots` nearest to `want`, at least one round.
+inline int64_t whole_rounds(int64_t want, int64_t slots) {
+  const int64_t k = std::max<int64_t>(1, (want + slots / 2) / slots);
+  return k * slots;
+}
+
 // share: this matrix's fraction of the elements of the whole call (the
 // large-rank grids are sized for the batch).
-inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0) {
+inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0,
+                          const Slots& sl = Slots{}) {
   Tiling t{};
   t.n_pad = (int)round_up(n, 32);
   t.m_pad = (int)round_up(m, 32);
@@ -143,14 +157,21 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0) {
     t.blocks[K_MHAT] = ctm * cdiv(m, t.mr);
     return t;
   }
-  // Grid sizes.  The split kernels aim at L_SPLIT_BLOCKS blocks over the
-  // whole batch, each matrix taking its share by element count (`share` =
-  // this matrix's fraction of the call's elements), but at least
-  // L_MIN_BLOCKS per matrix; each split adds a partial (rows x rank for the
-  // left product, summed by the Gram kernel; cols x rank for the right
-  // product), so splits stay at least L_MIN_COLS columns / L_MIN_ROWS rows
-  // wide.  The reconstruction has no partials and aims at twice as many.
-  const int64_t target = std::max<int64_t>(L_MIN_BLOCKS, (int64_t)(share * (double)L_SPLIT_BLOCKS + 0.5));
+  // Grid sizes.  The split kernels aim at about L_SPLIT_BLOCKS blocks over
+  // the whole batch (the reconstruction, which has no partials, at twice
+  // as many), rounded to whole rounds of resident blocks; each matrix takes
+  // its share by element count (`share` = this matrix's fraction of the
+  // call's elements), but at least a quarter round.  Each split adds a
+  // partial (rows x rank for the left product, summed by the Gram kernel;
+  // cols x rank for the right product), so splits stay at least L_MIN_COLS
+  // columns / L_MIN_ROWS rows wide.
+  auto target_of = [&](int64_t want, int64_t slots) {
+    const int64_t total = whole_rounds(want, slots);
+    return std::max<int64_t>(std::max<int64_t>(1, total / 4), (int64_t)(share * (double)total + 0.5));
+  };
+  const int64_t target = target_of(L_SPLIT_BLOCKS, sl.p);
+  const int64_t target_q = target_of(L_SPLIT_BLOCKS, sl.q);
+  const int64_t target_m = target_of(2 * L_SPLIT_BLOCKS, sl.m);
   // left product: 128-row tiles, columns split
   const int64_t row_tiles = cdiv(m, L_PROWS);
   const int64_t sp = clamp64(cdiv(target, row_tiles), 1, cdiv(n, L_MIN_COLS));
@@ -159,12 +180,12 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0) {
   t.ng = (int)cdiv(m, L_GROWS);
   // right product: column tiles, rows split
   const int64_t ctq = cdiv(n, lq_block_cols(rp));
-  const int64_t sq = clamp64(cdiv(target, ctq), 1, cdiv(m, L_MIN_ROWS));
+  const int64_t sq = clamp64(cdiv(target_q, ctq), 1, cdiv(m, L_MIN_ROWS));
   t.q_rows = (int)round_up(cdiv(m, sq), L_QG);
   t.sq = (int)cdiv(m, t.q_rows);
   // reconstruction: column tiles x row blocks (multiple of 32 rows)
   const int64_t ctm = cdiv(n, lm_block_cols(rp));
-  const int64_t rbm = clamp64(cdiv(2 * target, ctm), 1, cdiv(m, 32));
+  const int64_t rbm = clamp64(cdiv(target_m, ctm), 1, cdiv(m, 32));
   t.mr = (int)round_up(cdiv(m, rbm), 32);
   t.blocks[K_QPAD] = cdiv(t.n_pad, 8);    // 8-column tiles (k_qpadl)
   t.blocks[K_PASS_P] = row_tiles * t.sp;
