@@ -129,9 +129,13 @@ occ_status_t occ_compress(const void* M, int m_dtype, int64_t m, int64_t n, int6
                           int rank, int iters, void* ws, size_t ws_bytes,
                           occ_stream_t stream);
 
-/* Decompression (Sec. 9.6): M_hat = P Q^T with P m x rank and Q n x rank. */
+/* Decompression (Sec. 9.6): M_hat = P Q^T with P m x rank and Q n x rank.
+ * m_dtype names the dtype of the M the factors were computed from and selects
+ * the same products occ_step uses for it: for OCC_BF16 at ranks above 16 the
+ * factors are split into two bf16 parts each (about 2^-16 of |M_hat| per
+ * element, inside bf16 input precision), otherwise fp32 products. */
 occ_status_t occ_decompress(const float* P, const float* Q, int64_t m, int64_t n, int rank,
-                            float* M_hat, int64_t ldh, occ_stream_t stream);
+                            int m_dtype, float* M_hat, int64_t ldh, occ_stream_t stream);
 
 /* Error update (Sec. 5.1): err_new = (M + err_prev) - M_hat, elementwise.
  * err_new may equal err_prev (in place, same ld); err_prev NULL means zero. */

@@ -181,8 +181,12 @@ Slots device_slots_for(int dev) {
   else
     ok = ok && hipOccupancyMaxActiveBlocksPerMultiprocessor(&bq, k_lq<DT_F32, RP, SA_SAVED>,
                                                             kBlock, 0) == hipSuccess;
-  ok = ok && hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                 &bm, k_ml<DT_F32, RP, SA_SAVED, 0, true, true>, kBlock, 0) == hipSuccess;
+  if constexpr (X3)
+    ok = ok && hipOccupancyMaxActiveBlocksPerMultiprocessor(&bm, k_mlx<RP, 0, true, true>, kBlock,
+                                                            0) == hipSuccess;
+  else
+    ok = ok && hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                   &bm, k_ml<DT_F32, RP, SA_SAVED, 0, true, true>, kBlock, 0) == hipSuccess;
   if (!ok || bp < 1 || bq < 1 || bm < 1) {
     (void)hipGetLastError();
     return Slots{};
@@ -448,10 +452,18 @@ occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, h
           L("q_reduce", k_qredl<RP>, b.blocks[K_QRED]);
         }
         if (finish) {
-          if (write_mhat)
-            L("mhat_err_a", k_ml<DT_F32, RP, SA_SAVED, 0, true, true>, b.blocks[K_MHAT]);
-          else
-            L("err_only_a", k_ml<DT_F32, RP, SA_SAVED, 0, false, true>, b.blocks[K_MHAT]);
+          // bf16 M: the reconstruction on bf16 matrix cores with split operands
+          if constexpr (X3) {
+            if (write_mhat)
+              L("mhat_err_a", k_mlx<RP, 0, true, true>, b.blocks[K_MHAT]);
+            else
+              L("err_only_a", k_mlx<RP, 0, false, true>, b.blocks[K_MHAT]);
+          } else {
+            if (write_mhat)
+              L("mhat_err_a", k_ml<DT_F32, RP, SA_SAVED, 0, true, true>, b.blocks[K_MHAT]);
+            else
+              L("err_only_a", k_ml<DT_F32, RP, SA_SAVED, 0, false, true>, b.blocks[K_MHAT]);
+          }
         }
       }
     });
@@ -570,7 +582,8 @@ occ_status_t occ_compress(const void* M, int m_dtype, int64_t m, int64_t n, int6
 }
 
 occ_status_t occ_decompress(const float* P, const float* Q, int64_t m, int64_t n, int rank,
-                            float* M_hat, int64_t ldh, occ_stream_t stream) {
+                            int m_dtype, float* M_hat, int64_t ldh, occ_stream_t stream) {
+  if (m_dtype != OCC_F32 && m_dtype != OCC_BF16) return OCC_E_DTYPE;
   OCC_TRY(check_shape(m, n, ldh));
   if (rank < 1 || rank > OCC_MAX_RANK || rank > m || rank > n) return OCC_E_RANK;
   if (!P || !Q || !M_hat) return OCC_E_NULL;
@@ -596,10 +609,14 @@ occ_status_t occ_decompress(const float* P, const float* Q, int64_t m, int64_t n
     constexpr int RP = decltype(RPc)::value;
     st = launch("decompress", s, [&] {
       if constexpr (RP > kFusedMaxRank) {
-        // same products as the fused step's reconstruction pass
-        hipLaunchKernelGGL((k_ml<DT_F32, RP, SA_SAVED, 1, true, false>),
-                           dim3(grid_of(t.blocks[K_MHAT])), dim3(kBlock), 0, s,
-                           (const Desc*)nullptr, 1, d);
+        // same products as the fused step's reconstruction pass for this M dtype
+        if (m_dtype == OCC_BF16)
+          hipLaunchKernelGGL((k_mlx<RP, 1, true, false>), dim3(grid_of(t.blocks[K_MHAT])),
+                             dim3(kBlock), 0, s, (const Desc*)nullptr, 1, d);
+        else
+          hipLaunchKernelGGL((k_ml<DT_F32, RP, SA_SAVED, 1, true, false>),
+                             dim3(grid_of(t.blocks[K_MHAT])), dim3(kBlock), 0, s,
+                             (const Desc*)nullptr, 1, d);
       } else if (vec) {
         // same code as the fused step's reconstruction pass
         hipLaunchKernelGGL((k_mh16<DT_F32, true, RP, 1, true, false>),

@@ -1297,4 +1297,167 @@ __global__ __launch_bounds__(kBlock) void k_ml(OCC_KARGS) {
 #undef B_
 }
 
+// -------------------------------------------------------------------------
+// k_mlx: the reconstruction pass for bf16 M on the bf16 matrix cores with
+// split operands (as the products of k_lp X3): M_hat = P_hat Q^T accumulated
+// in fp32 as P_hi Q_hi + P_hi Q_lo + P_lo Q_hi on v_mfma_f32_32x32x16_bf16,
+// 16 ranks per K-step s, with
+//   A operand  P_hat: lane (g, li) supplies row li of the 32-row tile, ranks
+//              16 s + 8 g .. + 7, from an LDS tile of bf16 hi/lo rows staged
+//              from P_hat (SRC 0: the workspace copy; SRC 1: the caller's P,
+//              zero past rank r);
+//   B operand  Q^T: lane (g, li) supplies the same ranks of its column
+//              cw + 32 c + li, split once into bf16 hi/lo registers;
+// so acc[c][v] = M_hat[row0 + mf32_row(v, g)][cw + 32 c + li], the layout of
+// k_ml, and err = A - M_hat is formed and stored as there.  Rounding both
+// factors to two bf16 parts leaves about 2^-16 of |M_hat| per element, far
+// inside bf16 input precision; at rank 128 the pass needs 3/16 of the
+// matrix-core cycles of the fp32 form and is bound by memory instead.
+// -------------------------------------------------------------------------
+template <int RP>
+struct LMXSmem {
+  uint16_t p[2][2][32 * (RP + 8)];   // [stage][hi, lo][row][rank], pitch RP + 8
+};
+
+template <int RP, int SRC>
+__device__ __forceinline__ void lmx_fetch(const Desc& d, int row0, f4v* pr) {
+  constexpr int SF = RP * 8 / kBlock;   // float4s of a 32 x RP tile per thread
+#pragma unroll
+  for (int x = 0; x < SF; ++x) {
+    const int f = threadIdx.x + kBlock * x;
+    const int i = f / (RP / 4), k = 4 * (f % (RP / 4));
+    const int row = row0 + i;
+    f4v v = f4v{0.f, 0.f, 0.f, 0.f};
+    if (row < d.m) {
+      if (SRC == 0) {
+        v = *(const f4v*)(d.phat + (int64_t)row * RP + k);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (k + e < d.r) v[e] = d.P[(int64_t)row * d.r + k + e];
+      }
+    }
+    pr[x] = v;
+  }
+}
+
+template <int RP>
+__device__ __forceinline__ void lmx_stage(const f4v* pr, uint16_t (*dst)[32 * (RP + 8)]) {
+  constexpr int SF = RP * 8 / kBlock;
+#pragma unroll
+  for (int x = 0; x < SF; ++x) {
+    const int f = threadIdx.x + kBlock * x;
+    const int i = f / (RP / 4), k = 4 * (f % (RP / 4));
+    uint16_t hi[4], lo[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const __bf16 h = (__bf16)pr[x][e];
+      hi[e] = bf16_bits(h);
+      lo[e] = bf16_bits((__bf16)(pr[x][e] - (float)h));
+    }
+    const int off = i * (RP + 8) + k;
+    *(uint2*)(&dst[0][off]) = make_uint2(hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
+    *(uint2*)(&dst[1][off]) = make_uint2(lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16));
+  }
+}
+
+template <int RP, int SRC, bool WM, bool WE>
+__device__ __forceinline__ void lmx_body(const Desc& d, int b, LMXSmem<RP>& sm) {
+  constexpr int NCT = lm_tiles(RP), KS = RP / 16, BC = lm_block_cols(RP);
+  constexpr int SF = RP * 8 / kBlock;
+  constexpr int PT = RP + 8;
+  const int wave = wave_id(), lane = threadIdx.x & 63;
+  const int li = lane & 31, g = lane >> 5;
+  const int col_tiles = (d.n + BC - 1) / BC;
+  const int ct = b % col_tiles, rb = b / col_tiles;
+  const int r_lo = rb * d.mr, r_hi = min(d.m, r_lo + d.mr);
+  const int ntile = (r_hi - r_lo + 31) / 32;
+  const int cw = ct * BC + wave * 32 * NCT;
+
+  // Q^T operands: ranks 16 s + 8 g .. + 7 of column cw + 32 c + li
+  bf16x8 bh[NCT][KS], bl[NCT][KS];
+#pragma unroll
+  for (int c = 0; c < NCT; ++c) {
+    const int col = cw + 32 * c + li;
+#pragma unroll
+    for (int s2 = 0; s2 < KS; ++s2) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int k = 16 * s2 + 8 * g + e;
+        float v = 0.f;
+        if (SRC == 0) {
+          if (col < d.n_pad) v = d.qpad[(int64_t)col * RP + k];
+        } else {
+          if (col < d.n && k < d.r) v = d.Q[(int64_t)col * d.r + k];
+        }
+        const __bf16 h = (__bf16)v;
+        bh[c][s2][e] = h;
+        bl[c][s2][e] = (__bf16)(v - (float)h);
+      }
+    }
+  }
+
+  f4v pr[SF];
+  lmx_fetch<RP, SRC>(d, r_lo, pr);
+  lmx_stage<RP>(pr, sm.p[0]);
+  __syncthreads();
+
+  for (int tile = 0; tile < ntile; ++tile) {
+    const int row0 = r_lo + 32 * tile;
+    const bool more = tile + 1 < ntile;
+    if (more) lmx_fetch<RP, SRC>(d, row0 + 32, pr);
+    // A for this tile's outputs (issued before the products to hide latency)
+    RawA<DT_F32, SA_SAVED, 1> av[NCT][16];
+    if (WE) {
+#pragma unroll
+      for (int c = 0; c < NCT; ++c)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          av[c][v] = rawa_load<DT_F32, SA_SAVED, 1>(d, true, row0 + mf32_row(v, g), cw + 32 * c + li, d.n);
+    }
+    f16v acc[NCT];
+#pragma unroll
+    for (int c = 0; c < NCT; ++c) acc[c] = f16v{};
+    const uint16_t* ph = &sm.p[tile & 1][0][li * PT + 8 * g];
+    const uint16_t* pl = &sm.p[tile & 1][1][li * PT + 8 * g];
+#pragma unroll
+    for (int s2 = 0; s2 < KS; ++s2) {
+      const bf16x8 ah = *(const bf16x8*)(ph + 16 * s2);
+      const bf16x8 al = *(const bf16x8*)(pl + 16 * s2);
+#pragma unroll
+      for (int c = 0; c < NCT; ++c) {
+        acc[c] = mfma32bf(ah, bh[c][s2], acc[c]);
+        acc[c] = mfma32bf(ah, bl[c][s2], acc[c]);
+        acc[c] = mfma32bf(al, bh[c][s2], acc[c]);
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < NCT; ++c) {
+      const int col = cw + 32 * c + li;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = row0 + mf32_row(v, g);
+        if (row < r_hi && col < d.n) {
+          const float mh = acc[c][v];
+          if (WM) __builtin_nontemporal_store(mh, d.Mhat + (int64_t)row * d.ldh + col);
+          if (WE) {
+            const float e = rawa_val<DT_F32, SA_SAVED, 1>(av[c][v], 0) - mh;
+            __builtin_nontemporal_store(e, d.err_out + (int64_t)row * d.lde_out + col);
+          }
+        }
+      }
+    }
+    if (more) lmx_stage<RP>(pr, sm.p[(tile + 1) & 1]);
+    __syncthreads();
+  }
+}
+
+template <int RP, int SRC, bool WM, bool WE>
+__global__ __launch_bounds__(kBlock) void k_mlx(OCC_KARGS) {
+  __shared__ __attribute__((aligned(16))) LMXSmem<RP> sm;
+#define B_(d, b) lmx_body<RP, SRC, WM, WE>(d, b, sm)
+  OCC_DISPATCH(K_MHAT, B_)
+#undef B_
+}
+
 }  // namespace occ

@@ -85,8 +85,8 @@ _SIGS = {
                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
                                     ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "occ_decompress": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
-                                      ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
-                                      ctypes.c_int64, ctypes.c_void_p]),
+                                      ctypes.c_int64, ctypes.c_int, ctypes.c_int,
+                                      ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p]),
     "occ_err_update": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_int64,
                                       ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p,
                                       ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
@@ -293,15 +293,19 @@ def occ_compress(M, err_prev, Q, rank: int, iters: int, P=None, ws=None, stream=
     return P
 
 
-def occ_decompress(P, Q, M_hat=None, stream=None):
-    """M_hat = P Q^T."""
+def occ_decompress(P, Q, M_hat=None, m_dtype="f32", stream=None):
+    """M_hat = P Q^T, with the products occ_step uses for an M of dtype
+    m_dtype ("f32" or "bf16")."""
     torch = _torch()
     _f32(P, "P"), _f32(Q, "Q")
     m, rank = P.shape
     n = Q.shape[0]
+    if m_dtype not in ("f32", "bf16"):
+        raise ValueError(f"m_dtype must be 'f32' or 'bf16', not {m_dtype!r}")
     if M_hat is None:
         M_hat = torch.empty((m, n), dtype=torch.float32, device=P.device)
-    _check("occ_decompress", lib().occ_decompress(_ptr(P), _ptr(Q), m, n, rank, _ptr(M_hat),
+    _check("occ_decompress", lib().occ_decompress(_ptr(P), _ptr(Q), m, n, rank,
+                                                  1 if m_dtype == "bf16" else 0, _ptr(M_hat),
                                                   _ld(M_hat, "M_hat"), _stream(stream)))
     return M_hat
 

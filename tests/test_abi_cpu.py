@@ -87,9 +87,11 @@ def test_batched_errors(L):
 
 def test_other_entry_points_validate(L):
     # decompress: rank > n
-    assert L.occ_decompress(1 << 20, 1 << 21, 10, 3, 4, 1 << 22, 3, None) == 3
+    assert L.occ_decompress(1 << 20, 1 << 21, 10, 3, 4, 0, 1 << 22, 3, None) == 3
     # decompress: output overlaps P
-    assert L.occ_decompress(1 << 20, 1 << 24, 10, 8, 4, (1 << 20) + 8, 8, None) == 7
+    assert L.occ_decompress(1 << 20, 1 << 24, 10, 8, 4, 0, (1 << 20) + 8, 8, None) == 7
+    # decompress: unknown M dtype
+    assert L.occ_decompress(1 << 20, 1 << 24, 10, 8, 4, 2, 1 << 26, 8, None) == 5
     # err_update: in place needs equal leading dimensions
     assert L.occ_err_update(1 << 20, 0, 4, 4, 4, 1 << 24, 4, 1 << 26, 4, 1 << 24, 8, None) == 7
     # compress: missing workspace

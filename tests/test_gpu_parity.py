@@ -105,13 +105,14 @@ def test_unaligned_leading_dimension():
 @pytest.mark.parametrize("snr", [False, True])
 @pytest.mark.parametrize("rank", [32, 64, 128])
 def test_bf16_large_rank_split_products_accuracy(rank, snr):
-    """bf16 M at rank > 16 runs its left and right products on the bf16 matrix
-    cores with each operand split as x = x_hi + x_lo (x - x_hi - x_lo below
-    2^-16 |x|).  The split must keep the result close to fp32 arithmetic:
-    measured 1e-5 (noise-dominated) to 7e-5 (high SNR, where err is 1 % of A)
-    against the float64 oracle.  Dropping the lo parts would leave bf16
-    operands (2^-9 relative), about 2e-3 per product, so the bound 5e-4 -- well
-    inside the 2e-2 bf16 tolerance -- catches a broken split."""
+    """bf16 M at rank > 16 runs its left and right products and the
+    reconstruction on the bf16 matrix cores with each operand split as
+    x = x_hi + x_lo (x - x_hi - x_lo below 2^-16 |x|).  The split must keep the
+    result close to fp32 arithmetic: measured 1e-5 (noise-dominated) to 7e-5
+    (high SNR, where err is 1 % of A) against the float64 oracle with the
+    products split.  Dropping the lo parts would leave bf16 operands (2^-9
+    relative), about 2e-3 per product, so the bound 5e-4 -- well inside the
+    2e-2 bf16 tolerance -- catches a broken split."""
     w = WORKLOADS[5].scaled([(700, 520)], rank=rank, signal_rank=160)
     if snr:
         w = high_snr(w)

@@ -63,11 +63,32 @@ def test_fused_equals_unfused_bitwise(rank, dtype):
     Qb = Qa.clone()
     P1, Mh1 = optcc.occ_step(Md, err_a, Qa, rank, 2)
     P2 = optcc.occ_compress(Md, err_b, Qb, rank, 2)
-    Mh2 = optcc.occ_decompress(P2, Qb)
+    Mh2 = optcc.occ_decompress(P2, Qb, m_dtype=dtype)
     optcc.occ_err_update(Md, err_b, Mh2, err_new=err_b)
     torch.cuda.synchronize()
     for x, y in ((P1, P2), (Qa, Qb), (Mh1, Mh2), (err_a, err_b)):
         assert torch.equal(x.view(torch.int32), y.view(torch.int32))
+
+
+@pytest.mark.parametrize("rank", [40, 128])
+def test_split_decompress_close_to_fp32(rank):
+    """occ_decompress for bf16 M above rank 16 uses the split bf16 products of
+    the fused step (two bf16 parts per factor, about 2^-16 relative per
+    element); the fp32 form stays at fp32 rounding.  Both against float64."""
+    from paper_2301_09830_amd import optcc
+    torch = torch_mod()
+    g = torch.Generator(device="cuda").manual_seed(3)
+    P = torch.randn((700, rank), device="cuda", generator=g)
+    Q = torch.randn((260, rank), device="cuda", generator=g)
+    ref = P.double() @ Q.double().T
+    a = optcc.occ_decompress(P, Q, m_dtype="f32")
+    b = optcc.occ_decompress(P, Q, m_dtype="bf16")
+    torch.cuda.synchronize()
+    rel_a = ((a.double() - ref).norm() / ref.norm()).item()
+    rel_b = ((b.double() - ref).norm() / ref.norm()).item()
+    print(f"[decompress] rank {rank}: fp32 {rel_a:.2e}, split bf16 {rel_b:.2e}", flush=True)
+    assert rel_a <= 1e-6
+    assert rel_b <= 1e-4
 
 
 @pytest.mark.parametrize("rank", [8, 64])
