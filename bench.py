@@ -98,8 +98,9 @@ def step_alg_bytes(elements: int, m_bytes: int, iters: int, write_mhat: bool = T
     return elements * min(x, y)
 
 
-def load_traffic(kernel: str, workload: str, launches_elements: int):
-    """HBM bytes per launch from the committed counter summary, or None."""
+def load_profile(kernel: str, workload: str) -> dict | None:
+    """The committed counter summary of a kernel on a workload, if it was
+    taken on the current kernel sources."""
     path = os.path.join(PROFILES, f"{kernel}__{workload}__pmc.md")
     if not os.path.exists(path):
         return None
@@ -114,7 +115,13 @@ def load_traffic(kernel: str, workload: str, launches_elements: int):
         return None
     if rec.get("kernel_source_sha") != kernel_source_digest():
         return None
-    return rec.get("hbm_bytes_per_launch")
+    return rec
+
+
+def load_traffic(kernel: str, workload: str, launches_elements: int):
+    """HBM bytes per launch from the committed counter summary, or None."""
+    rec = load_profile(kernel, workload)
+    return None if rec is None else rec.get("hbm_bytes_per_launch")
 
 
 # ----------------------------------------------------------------------------
@@ -196,6 +203,10 @@ def profile_name(kname: str) -> str | None:
         if args[3] == "1":
             return "decompress"
         return "mhat_err_a" if args[4] == "true" else "err_only_a"
+    if short == "k_mlx":
+        if args[1] == "1":
+            return "decompress"
+        return "mhat_err_a" if args[2] == "true" else "err_only_a"
     if short == "k_lqx":
         return {"0": "pass_q", "2": "pass_q_a"}[args[2]]
     pair = {"k_lg": "gram", "k_gsum": "gram_sum", "k_lchol": "chol", "k_lapply": "apply"}
@@ -204,9 +215,15 @@ def profile_name(kname: str) -> str | None:
     return None
 
 
+XCDS = 8        # accelerator complex dies of the MI355X (GRBM_GUI_ACTIVE is summed over them)
+SIMDS = 1024    # 256 compute units x 4 SIMDs
+
+
 def write_profiles(workload: str, trace_dir: str, fetch_dir: str, write_dir: str,
-                   commands: dict, elements: int, m_bytes: int) -> list:
-    """Summaries of one rocprofv3 kernel trace and two counter runs."""
+                   commands: dict, elements: int, m_bytes: int, mfma_dir: str | None = None,
+                   streaming_only: bool = False) -> list:
+    """Summaries of one rocprofv3 kernel trace and two counter runs (plus, with
+    mfma_dir, a run of matrix-core counters)."""
     import csv
     out = []
     stats = glob.glob(os.path.join(trace_dir, "*kernel_stats.csv"))[0]
@@ -222,6 +239,12 @@ def write_profiles(workload: str, trace_dir: str, fetch_dir: str, write_dir: str
             agg.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
         return {k: sum(v) / len(v) for k, v in agg.items()}
     fetch, write = counters(fetch_dir), counters(write_dir)
+    mf = {}
+    if mfma_dir:
+        for r in csv.DictReader(open(glob.glob(os.path.join(mfma_dir, "*counter_collection.csv"))[0])):
+            mf.setdefault(r["Kernel_Name"].split("(")[0], {}).setdefault(r["Counter_Name"], []).append(
+                float(r["Counter_Value"]))
+        mf = {k: {c: sum(v) / len(v) for c, v in d.items()} for k, d in mf.items()}
     copy = [k for k in fetch if "copyBuffer" in k or "copy" in k.lower()]
     cal_read = cal_write = None
     calib_bytes = commands.get("calibration_bytes")
@@ -232,7 +255,7 @@ def write_profiles(workload: str, trace_dir: str, fetch_dir: str, write_dir: str
     digest = kernel_source_digest()
     for r in rows:
         name = profile_name(r["Name"])
-        if name is None:
+        if name is None or (streaming_only and kernel_alg_bytes(name, 1, m_bytes) is None):
             continue
         fk = next((k for k in fetch if k.split("(")[0] == r["Name"].split("(")[0]), None)
         rec = {"kernel": name, "hip_kernel": r["Name"].split("(")[0], "workload": workload,
@@ -247,12 +270,27 @@ def write_profiles(workload: str, trace_dir: str, fetch_dir: str, write_dir: str
             alg = kernel_alg_bytes(name, elements, m_bytes)
             if alg:
                 rec["alg_bytes_per_launch"] = alg
+        mk = mf.get(r["Name"].split("(")[0])
+        if mk and mk.get("GRBM_GUI_ACTIVE"):
+            busy = mk.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+            gui = mk["GRBM_GUI_ACTIVE"]
+            mops = sum(mk.get(c, 0.0) for c in ("SQ_INSTS_VALU_MFMA_MOPS_F32", "SQ_INSTS_VALU_MFMA_MOPS_BF16",
+                                                   "SQ_INSTS_VALU_MFMA_MOPS_F64"))
+            rec["mfma"] = {
+                "busy_cycles": busy, "gui_active": gui,
+                "util": round(busy / (gui / XCDS * SIMDS), 4),
+                "flops_per_launch": mops * 512,
+                "mops_f32": mk.get("SQ_INSTS_VALU_MFMA_MOPS_F32", 0.0),
+                "mops_bf16": mk.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0),
+                "mops_f64": mk.get("SQ_INSTS_VALU_MFMA_MOPS_F64", 0.0),
+                "tflops": round(mops * 512 / (rec["avg_duration_us"] * 1e-6) / 1e12, 1)}
         text = [f"# `{name}` on {workload}: rocprofv3 summary", "",
                 f"Kernel `{rec['hip_kernel']}`; average duration {rec['avg_duration_us']} us "
                 f"over {r['Calls']} dispatches.", "",
                 "Commands (run from the repository root on the MI355X box):", ""]
-        for key in ("trace", "fetch", "write"):
-            text.append(f"- {key}: `{commands[key]}`")
+        for key in ("trace", "fetch", "write", "mfma"):
+            if key in commands:
+                text.append(f"- {key}: `{commands[key]}`")
         text += ["", "Kernel trace statistics of the same run (all kernels of the step):", ""] + lines
         if "hbm_bytes_per_launch" in rec:
             text += ["", f"HBM traffic per dispatch: FETCH_SIZE {rec['fetch_kib_per_dispatch']} KiB x "
@@ -260,6 +298,13 @@ def write_profiles(workload: str, trace_dir: str, fetch_dir: str, write_dir: str
                          f"{rec['write_calibration']} = {rec['hbm_bytes_per_launch']} bytes. The calibration "
                          "factors are (bytes a plain device copy of known size moves) / (what the counter "
                          "reports for that copy)."]
+        if "mfma" in rec:
+            m_ = rec["mfma"]
+            text += ["", f"Matrix cores: SQ_VALU_MFMA_BUSY_CYCLES {m_['busy_cycles']:.0f} over GRBM_GUI_ACTIVE "
+                         f"{m_['gui_active']:.0f} (summed over the {XCDS} XCDs) and {SIMDS} SIMDs: busy "
+                         f"{100 * m_['util']:.1f} % of the kernel's cycles; MFMA MOPS x 512 = "
+                         f"{m_['flops_per_launch'] / 1e9:.1f} GFLOP per dispatch of matrix-core work, "
+                         f"{m_['tflops']} TFLOP/s over the average duration."]
         text += ["", "```json", json.dumps(rec, indent=1), "```", ""]
         path = os.path.join(PROFILES, f"{name}__{workload}__pmc.md")
         with open(path, "w") as f:
@@ -281,6 +326,8 @@ def main() -> int:
     ap.add_argument("--no-kernel-timing", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this size (counter calibration)")
+    ap.add_argument("--mfma-dir", default=None,
+                    help="with --write-profiles: rocprofv3 csv output of the matrix-core counter run")
     ap.add_argument("--write-profiles", nargs=3, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR"),
                     help="host only: turn rocprofv3 csv output into profiles/*.md summaries")
     ap.add_argument("--profile-commands", default="",
@@ -291,7 +338,8 @@ def main() -> int:
         from workloads import WORKLOADS
         w = WORKLOADS[args.workload]
         paths = write_profiles(w.name, *args.write_profiles, json.loads(args.profile_commands),
-                               w.elements, 2 if w.m_dtype == "bf16" else 4)
+                               w.elements, 2 if w.m_dtype == "bf16" else 4, mfma_dir=args.mfma_dir,
+                               streaming_only=w.rank > 16)
         print("\n".join(paths))
         return 0
 
@@ -378,7 +426,8 @@ def main() -> int:
             avg_s = total_ms / launches * 1e-3
             per_launch = kernel_alg_bytes(dom, elements, m_bytes)  # one launch covers the batch
             flops = kernel_alg_flops(dom, elements, w.rank)
-            traffic = load_traffic(dom, w.name, elements)
+            prof_rec = load_profile(dom, w.name)
+            traffic = None if prof_rec is None else prof_rec.get("hbm_bytes_per_launch")
             # the bound is whichever resource the kernel's algorithmic work
             # needs longer on: HBM bytes at 8 TB/s or its flops on the matrix
             # cores it runs on
@@ -393,6 +442,7 @@ def main() -> int:
                         "frac": round(achieved / peak, 4),
                         "traffic": traffic, "alg_bytes_per_launch": int(per_launch),
                         "alg_flops_per_launch": flops, "engine": engine,
+                        "mfma_util": (prof_rec or {}).get("mfma", {}).get("util"),
                         "hbm_achieved_gbs": round(per_launch / avg_s / 1e9, 1),
                         "avg_launch_us": round(avg_s * 1e6, 3)}
 
