@@ -126,11 +126,92 @@ __device__ __forceinline__ Q8v q8_load(const float* qs, int n, int c, int li) {
 // stream contiguous column ranges) and their partial tiles are summed in LDS
 // in wave order.  The block then stores its final rows of P and the fp64
 // Gram partial of those rows.
+//
+// The MFMA operand layout gives each of a load's 64 lanes a different row
+// out of 16 (4 lanes x 16 bytes per row), so a load straight into registers
+// touches 16 cache lines per instruction, half of each, and the other half
+// comes with the next instruction; the L1 address path then stalls the
+// texture addresser for about half of the kernel.  With 16-byte aligned
+// rows the tiles are instead brought in by global_load_lds_dwordx4, which
+// writes lane l's 16 bytes to LDS at base + 16 l and so lets every
+// instruction read whole 128-byte lines (8 rows of err, 16 rows of bf16 M);
+// lanes fetch their chunks in an XOR-swizzled order so that the operand
+// reads from LDS are free of bank conflicts.  Each wave owns two tile
+// stages: it waits for the K-step it is about to use, reads its operands,
+// and issues the next K-step's tile before running the products.
 // -------------------------------------------------------------------------
-struct PMSmem {
-  float red[PM_WAVES][PM_ROWS * 16];   // per-wave partial tiles
-  double rows[PM_ROWS * 16];           // final P rows as doubles (Gram)
+constexpr int PM_ESLOT = 1024 + 128;   // LDS bytes per 8-row err load; the pad shifts banks by 32 words
+constexpr int PM_BSLOT = 1024;         // LDS bytes per 16-row bf16 M load
+constexpr int PM_QBYTES = 32 * 16 * 4; // Q rows of a K-step (rank padded to at most 16)
+constexpr int PM_STAGE = 4 * PM_ESLOT + 2 * PM_BSLOT + PM_QBYTES;   // one K-step, 32 rows x 32 columns
+
+union PMSmem {
+  struct {
+    float red[PM_WAVES][PM_ROWS * 16];   // per-wave partial tiles
+    double rows[PM_ROWS * 16];           // final P rows as doubles (Gram)
+  } e;
+  uint8_t tile[PM_WAVES][2][PM_STAGE];   // per wave, two K-step stages (bf16 M)
 };
+
+typedef __attribute__((address_space(1))) void gvoid_t;
+typedef __attribute__((address_space(3))) void lvoid_t;
+
+// K-step columns [c0, c0 + 32) of the block's 32 rows of err and bf16 M, and
+// Q rows c0 .. c0+31, into `dst` (rows past m repeat row m-1; their results
+// are never stored).
+template <int RP>
+__device__ __forceinline__ void pm_tile_issue(const Desc& d, const float* qs, int row0, int c0,
+                                              uint8_t* dst) {
+  const int lane = threadIdx.x & 63;
+  const int last = d.m - 1;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    // err rows 8q .. 8q+7: lane l takes row l / 8, chunk (l % 8) ^ (l / 8)
+    const int rr = lane >> 3, ch = (lane & 7) ^ rr;
+    const int row = min(row0 + 8 * q + rr, last);
+    __builtin_amdgcn_global_load_lds((gvoid_t*)(d.err_in + (int64_t)row * d.lde_in + c0 + 4 * ch),
+                                     (lvoid_t*)(dst + q * PM_ESLOT), 16, 0, 0);
+  }
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    // bf16 M rows 16q .. 16q+15: lane l takes row l / 4, chunk (l % 4) ^ (l / 16)
+    const int rr = lane >> 2, ch = (lane & 3) ^ (rr >> 2);
+    const int row = min(row0 + 16 * q + rr, last);
+    __builtin_amdgcn_global_load_lds((gvoid_t*)((const uint16_t*)d.M + (int64_t)row * d.ldm + c0 + 8 * ch),
+                                     (lvoid_t*)(dst + 4 * PM_ESLOT + q * PM_BSLOT), 16, 0, 0);
+  }
+  // Q rows c0 .. c0+31 (32 RP floats, contiguous) as they are
+#pragma unroll
+  for (int q = 0; q < (32 * RP * 4 + 1023) / 1024; ++q)
+    if (1024 * q + 16 * lane < 32 * RP * 4)
+      __builtin_amdgcn_global_load_lds((gvoid_t*)(qs + (int64_t)c0 * RP + 256 * q + 4 * lane),
+                                       (lvoid_t*)(dst + 4 * PM_ESLOT + 2 * PM_BSLOT + 1024 * q), 16, 0, 0);
+}
+
+// Lane (g, li)'s operand chunk of row tile r (row 16 r + li, columns 8g..8g+7)
+// from a tile written by pm_tile_issue.
+__device__ __forceinline__ Ch8<DT_BF16> pm_tile_read(const uint8_t* src, int r, int li, int g) {
+  Ch8<DT_BF16> x;
+  const int q = 2 * r + (li >> 3), rr = li & 7;
+  const uint8_t* e = src + q * PM_ESLOT + rr * 128;
+  x.e0 = *(const float4*)(e + 16 * ((2 * g) ^ rr));
+  x.e1 = *(const float4*)(e + 16 * ((2 * g + 1) ^ rr));
+  x.m = *(const uint4*)(src + 4 * PM_ESLOT + r * PM_BSLOT + li * 64 + 16 * (g ^ (li >> 2)));
+  return x;
+}
+
+// Q[c0 + 8g + j][li] for j < 8 from the tile (zero past the padded rank).
+template <int RP>
+__device__ __forceinline__ Q8v pm_tile_q(const uint8_t* src, int li, int g) {
+  const float* qt = (const float*)(src + 4 * PM_ESLOT + 2 * PM_BSLOT);
+  float v[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) v[j] = li < RP ? qt[(8 * g + j) * RP + li] : 0.f;
+  Q8v q;
+  q.a = make_float4(v[0], v[1], v[2], v[3]);
+  q.b = make_float4(v[4], v[5], v[6], v[7]);
+  return q;
+}
 
 template <int DT, bool VEC, int RP>
 __device__ __forceinline__ void pm_body(const Desc& d, int b, PMSmem& sm) {
@@ -154,55 +235,87 @@ __device__ __forceinline__ void pm_body(const Desc& d, int b, PMSmem& sm) {
 #pragma unroll
   for (int r = 0; r < PM_RB; ++r) acc[r] = f4v{0.f, 0.f, 0.f, 0.f};
 
-  Ch8<DT> cur[PM_RB], nxt[PM_RB];
-  Q8v cq, nq;
-  int ks = wave;
-  if (ks < nk) {
-    const int c = kcol(ks);
-    cq = q8_load<RP>(qs, d.n, c, li);
-#pragma unroll
-    for (int r = 0; r < PM_RB; ++r) cur[r] = ch8_load<DT, VEC>(d, row0 + 16 * r + li, c, d.n);
-  }
-  for (; ks < nk; ks += PM_WAVES) {
-    const bool more = ks + PM_WAVES < nk;
-    const int cn = more ? kcol(ks + PM_WAVES) : 0;
-    if (more) {
-      nq = q8_load<RP>(qs, d.n, cn, li);
-#pragma unroll
-      for (int r = 0; r < PM_RB; ++r) nxt[r] = ch8_load<DT, VEC>(d, row0 + 16 * r + li, cn, d.n);
-    }
+  auto mfma_step = [&](const Ch8<DT>* x, const Q8v& cq) {
     const float qv[8] = {cq.a.x, cq.a.y, cq.a.z, cq.a.w, cq.b.x, cq.b.y, cq.b.z, cq.b.w};
 #pragma unroll
     for (int r = 0; r < PM_RB; ++r) {
       float a[8];
-      ch8_values<DT>(cur[r], a);
+      ch8_values<DT>(x[r], a);
 #pragma unroll
       for (int j = 0; j < 8; ++j) acc[r] = mfma4(a[j], qv[j], acc[r]);
     }
-    if (more) {
-      cq = nq;
-#pragma unroll
-      for (int r = 0; r < PM_RB; ++r) cur[r] = nxt[r];
+  };
+
+  // bf16 M with 16-byte aligned rows, whole 32-column K-steps and a 16-byte
+  // aligned Q: tiles through LDS (the condition is the same for the whole
+  // launch); otherwise loads straight into registers.
+  bool dma = false;
+  if constexpr (DT == DT_BF16 && VEC) {
+    dma = d.err_in != nullptr && (d.n & 31) == 0 && ((uintptr_t)qs & 15) == 0;
+    if (dma) {
+      // stage s of this wave's tiles: its own base plus s * PM_STAGE (plain
+      // offsets keep the accesses in the LDS address space)
+      uint8_t* const tiles = sm.tile[wave][0];
+      int ks = wave;
+      if (ks < nk) pm_tile_issue<RP>(d, qs, row0, kcol(ks) - 8 * g, tiles);
+      for (int it = 0; ks < nk; ks += PM_WAVES, ++it) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        const uint8_t* cur = tiles + (it & 1) * PM_STAGE;
+        Ch8<DT> x[PM_RB];
+  #pragma unroll
+        for (int r = 0; r < PM_RB; ++r) x[r] = pm_tile_read(cur, r, li, g);
+        const Q8v cq = pm_tile_q<RP>(cur, li, g);
+        const int kn = ks + PM_WAVES;
+        if (kn < nk) pm_tile_issue<RP>(d, qs, row0, kcol(kn) - 8 * g, tiles + ((it + 1) & 1) * PM_STAGE);
+        mfma_step(x, cq);
+    }
     }
   }
+  if (!dma) {
+    Ch8<DT> cur[PM_RB], nxt[PM_RB];
+    Q8v cq, nq;
+    int ks = wave;
+    if (ks < nk) {
+      const int c = kcol(ks);
+      cq = q8_load<RP>(qs, d.n, c, li);
+#pragma unroll
+      for (int r = 0; r < PM_RB; ++r) cur[r] = ch8_load<DT, VEC>(d, row0 + 16 * r + li, c, d.n);
+    }
+    for (; ks < nk; ks += PM_WAVES) {
+      const bool more = ks + PM_WAVES < nk;
+      const int cn = more ? kcol(ks + PM_WAVES) : 0;
+      if (more) {
+        nq = q8_load<RP>(qs, d.n, cn, li);
+#pragma unroll
+        for (int r = 0; r < PM_RB; ++r) nxt[r] = ch8_load<DT, VEC>(d, row0 + 16 * r + li, cn, d.n);
+      }
+      mfma_step(cur, cq);
+      if (more) {
+        cq = nq;
+#pragma unroll
+        for (int r = 0; r < PM_RB; ++r) cur[r] = nxt[r];
+      }
+    }
+  }
+  __syncthreads();   // every wave is done with its tiles before they turn into the reduction buffer
 
   // acc[r][v] = partial P[row0 + 16r + 4g + v][li] of this wave.
 #pragma unroll
   for (int r = 0; r < PM_RB; ++r)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) sm.red[wave][(16 * r + 4 * g + v) * 16 + li] = acc[r][v];
+    for (int v = 0; v < 4; ++v) sm.e.red[wave][(16 * r + 4 * g + v) * 16 + li] = acc[r][v];
   __syncthreads();
   const int nr = min(PM_ROWS, d.m - row0);
   for (int e = threadIdx.x; e < PM_ROWS * RP; e += PM_THREADS) {
     const int i = e / RP, k = e % RP;
-    float s = sm.red[0][i * 16 + k];
+    float s = sm.e.red[0][i * 16 + k];
 #pragma unroll
-    for (int w = 1; w < PM_WAVES; ++w) s = s + sm.red[w][i * 16 + k];
+    for (int w = 1; w < PM_WAVES; ++w) s = s + sm.e.red[w][i * 16 + k];
     if (i < nr) d.praw[(int64_t)(row0 + i) * RP + k] = s;
-    sm.rows[i * RP + k] = (i < nr) ? (double)s : 0.0;
+    sm.e.rows[i * RP + k] = (i < nr) ? (double)s : 0.0;
   }
   __syncthreads();
-  gram_rows_store<RP, PM_THREADS>(sm.rows, nr, d.gpart + (int64_t)b * (RP * (RP + 1) / 2));
+  gram_rows_store<RP, PM_THREADS>(sm.e.rows, nr, d.gpart + (int64_t)b * (RP * (RP + 1) / 2));
 }
 
 template <int DT, bool VEC, int RP>

@@ -47,6 +47,17 @@ def test_rank_sweep_bf16(rank):
     assert_parity(res, "bf16", f"bf16 600x333 r{rank}")
 
 
+@pytest.mark.parametrize("shape", [(1000, 512), (77, 32), (300, 96), (4100, 224)])
+@pytest.mark.parametrize("rank", [3, 8, 16])
+def test_bf16_whole_ksteps_lds_tiles(shape, rank):
+    """bf16 M whose width is a multiple of 32 columns takes the left product's
+    LDS-tile path: ragged rows, fewer K-steps than waves, padded and unpadded
+    ranks."""
+    w = WORKLOADS[2].scaled([shape], rank=rank)
+    res, _, _ = run_workload(w, 2)
+    assert_parity(res, "bf16", f"bf16 {shape[0]}x{shape[1]} r{rank} (LDS tiles)")
+
+
 def test_config3_stage_batched_small():
     shapes = [(3 * 96, 96), (96, 96), (4 * 96, 96), (96, 4 * 96)] * 2
     w = WORKLOADS[3].scaled(shapes)
