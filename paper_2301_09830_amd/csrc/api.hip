@@ -173,8 +173,8 @@ Slots device_slots_for(int dev) {
   }
   constexpr bool X3 = DT == DT_BF16;
   int bp = 0, bq = 0, bm = 0;
-  bool ok = hipOccupancyMaxActiveBlocksPerMultiprocessor(&bp, k_lp<DT, RP, SA_MERR_SAVE, X3>,
-                                                         kBlock, 0) == hipSuccess;
+  bool ok = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                 &bp, k_lp<DT, RP, SA_MERR_SAVE, X3, true>, kBlock, 0) == hipSuccess;
   if constexpr (X3)
     ok = ok && hipOccupancyMaxActiveBlocksPerMultiprocessor(&bq, k_lqx<DT_F32, RP, SA_SAVED>,
                                                             kBlock, 0) == hipSuccess;
@@ -422,14 +422,29 @@ occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, h
         const bool saved = b.descs[0].err_out != nullptr;
         // bf16 M: left products on bf16 matrix cores with split operands
         constexpr bool X3 = DT == DT_BF16;
+        // left products with their A tiles through LDS when every row is
+        // 16-byte aligned, every 32-column K-step whole and A has a source
+        bool whole = VEC;
+        for (const Desc& dd : b.descs) whole = whole && dd.n % 32 == 0;
+        const bool tiles_merr = whole && b.descs[0].err_in != nullptr;
         L("qpad", k_qpadl<RP>, b.blocks[K_QPAD]);
         for (int it = 0; it < b.iters; ++it) {
-          if (!saved)
-            L("pass_p", k_lp<DT, RP, SA_MERR, X3>, b.blocks[K_PASS_P]);
-          else if (it == 0)
-            L("pass_p_first", k_lp<DT, RP, SA_MERR_SAVE, X3>, b.blocks[K_PASS_P]);
-          else
-            L("pass_p_a", k_lp<DT_F32, RP, SA_SAVED, X3>, b.blocks[K_PASS_P]);
+          if (!saved) {
+            if (tiles_merr)
+              L("pass_p", k_lp<DT, RP, SA_MERR, X3, true>, b.blocks[K_PASS_P]);
+            else
+              L("pass_p", k_lp<DT, RP, SA_MERR, X3, false>, b.blocks[K_PASS_P]);
+          } else if (it == 0) {
+            if (tiles_merr)
+              L("pass_p_first", k_lp<DT, RP, SA_MERR_SAVE, X3, true>, b.blocks[K_PASS_P]);
+            else
+              L("pass_p_first", k_lp<DT, RP, SA_MERR_SAVE, X3, false>, b.blocks[K_PASS_P]);
+          } else {
+            if (whole)
+              L("pass_p_a", k_lp<DT_F32, RP, SA_SAVED, X3, true>, b.blocks[K_PASS_P]);
+            else
+              L("pass_p_a", k_lp<DT_F32, RP, SA_SAVED, X3, false>, b.blocks[K_PASS_P]);
+          }
           L("gram", k_lg<RP, 0>, b.blocks[K_PGRAM]);
           L("gram_sum", k_gsum<RP, 0>, b.blocks[K_GSUM]);
           LB("chol", k_lchol<RP, 0>, count, LC_THREADS, flags);

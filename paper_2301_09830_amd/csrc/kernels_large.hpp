@@ -226,9 +226,136 @@ __device__ __forceinline__ f16v mfma32bf(bf16x8 a, bf16x8 b, f16v c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-template <int DT, int RP, int SA, bool X3>
+// A tiles of the left product through LDS (16-byte aligned rows, whole
+// 32-column K-steps).  With A fed straight from registers, lane li of a
+// 32x32 operand owns row li, so each load instruction touches 32 rows with
+// 32 bytes each and every 128-byte line is requested four times; the L1
+// address path then stalls the texture addresser for 40-70 % of the pass.
+// global_load_lds_dwordx4 writes lane l's 16 bytes to LDS at base + 16 l, so
+// a wave brings its 32 x 32 tile in with whole lines per instruction (8 rows
+// x 128 bytes of fp32, 16 rows x 64 bytes of bf16), lanes taking their
+// chunks in an XOR-swizzled order so that the operand reads (lane (g, li):
+// row li, columns 16g..16g+15) are free of bank conflicts.  Two stages per
+// wave: the wave reads its operands, issues the next K-step's tile, then
+// runs the products.  The stored A of a first pass is written from the
+// tile in the same whole-line order.
+constexpr int LP_ESLOT = 1024 + 128;   // 8 rows x 128 B of fp32; the pad shifts banks by 32 words
+constexpr int LP_BSLOT = 1024;         // 16 rows x 64 B of bf16
+template <int DT, int SA>
+struct LPTile {
+  static constexpr int A_BYTES = 4 * LP_ESLOT;   // err (or the stored A)
+  static constexpr int M_BYTES = SA == SA_SAVED ? 0 : (DT == DT_BF16 ? 2 * LP_BSLOT : 4 * LP_ESLOT);
+  static constexpr int BYTES = A_BYTES + M_BYTES;
+};
+
+template <int DT, int SA>
+__device__ __forceinline__ void lp_tile_issue(const Desc& d, int row0, int c0, uint8_t* dst) {
+  const int lane = threadIdx.x & 63;
+  const int last = d.m - 1;
+  const float* asrc = SA == SA_SAVED ? d.err_out : d.err_in;
+  const int64_t lda = SA == SA_SAVED ? d.lde_out : d.lde_in;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    // rows 8q .. 8q+7: lane l takes row l / 8, chunk (l % 8) ^ (l / 8)
+    const int rr = lane >> 3, ch = (lane & 7) ^ rr;
+    const int row = min(row0 + 8 * q + rr, last);
+    __builtin_amdgcn_global_load_lds((gvoid_t*)(asrc + (int64_t)row * lda + c0 + 4 * ch),
+                                     (lvoid_t*)(dst + q * LP_ESLOT), 16, 0, 0);
+  }
+  if constexpr (SA != SA_SAVED) {
+    uint8_t* mdst = dst + LPTile<DT, SA>::A_BYTES;
+    if constexpr (DT == DT_BF16) {
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        // rows 16q .. 16q+15: lane l takes row l / 4, chunk (l % 4) ^ (l / 16)
+        const int rr = lane >> 2, ch = (lane & 3) ^ (rr >> 2);
+        const int row = min(row0 + 16 * q + rr, last);
+        __builtin_amdgcn_global_load_lds(
+            (gvoid_t*)((const uint16_t*)d.M + (int64_t)row * d.ldm + c0 + 8 * ch),
+            (lvoid_t*)(mdst + q * LP_BSLOT), 16, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int rr = lane >> 3, ch = (lane & 7) ^ rr;
+        const int row = min(row0 + 8 * q + rr, last);
+        __builtin_amdgcn_global_load_lds(
+            (gvoid_t*)((const float*)d.M + (int64_t)row * d.ldm + c0 + 4 * ch),
+            (lvoid_t*)(mdst + q * LP_ESLOT), 16, 0, 0);
+      }
+    }
+  }
+}
+
+// A[row li][columns 16g .. 16g+15] of a tile (the values rawa_val gives).
+template <int DT, int SA>
+__device__ __forceinline__ void lp_tile_read(const uint8_t* src, int li, int g, float a[16]) {
+  const int q = li >> 3, rr = li & 7;
+  const uint8_t* e = src + q * LP_ESLOT + rr * 128;
+  float ev[16];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const float4 v = *(const float4*)(e + 16 * ((4 * g + t) ^ rr));
+    ev[4 * t] = v.x; ev[4 * t + 1] = v.y; ev[4 * t + 2] = v.z; ev[4 * t + 3] = v.w;
+  }
+  if constexpr (SA == SA_SAVED) {
+#pragma unroll
+    for (int j = 0; j < 16; ++j) a[j] = ev[j];
+  } else if constexpr (DT == DT_BF16) {
+    const int qb = li >> 4, rb = li & 15;
+    const uint8_t* m = src + LPTile<DT, SA>::A_BYTES + qb * LP_BSLOT + rb * 64;
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const uint4 w = *(const uint4*)(m + 16 * ((2 * g + t) ^ (rb >> 2)));
+      const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        a[8 * t + 2 * k] = bf16_lo(ww[k]) + ev[8 * t + 2 * k];
+        a[8 * t + 2 * k + 1] = bf16_hi(ww[k]) + ev[8 * t + 2 * k + 1];
+      }
+    }
+  } else {
+    const uint8_t* m = src + LPTile<DT, SA>::A_BYTES + q * LP_ESLOT + rr * 128;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const float4 v = *(const float4*)(m + 16 * ((4 * g + t) ^ rr));
+      a[4 * t] = v.x + ev[4 * t]; a[4 * t + 1] = v.y + ev[4 * t + 1];
+      a[4 * t + 2] = v.z + ev[4 * t + 2]; a[4 * t + 3] = v.w + ev[4 * t + 3];
+    }
+  }
+}
+
+// First pass: A = M + err_prev of the wave's tile stored over err, each lane
+// taking its own tile slots (whole 128-byte lines per store instruction).
+template <int DT>
+__device__ __forceinline__ void lp_tile_store_a(const Desc& d, const uint8_t* src, int row0, int c0) {
+  const int lane = threadIdx.x & 63;
+  const int rr = lane >> 3, ch = (lane & 7) ^ rr;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int r = 8 * q + rr;          // row within the wave's 32
+    const float4 e = *(const float4*)(src + q * LP_ESLOT + 16 * lane);
+    float a[4];
+    if constexpr (DT == DT_BF16) {
+      const int qb = r >> 4, rb = r & 15;
+      const uint2 w = *(const uint2*)(src + LPTile<DT, SA_MERR_SAVE>::A_BYTES + qb * LP_BSLOT + rb * 64 +
+                                      16 * ((ch >> 1) ^ (rb >> 2)) + 8 * (ch & 1));
+      a[0] = bf16_lo(w.x) + e.x; a[1] = bf16_hi(w.x) + e.y;
+      a[2] = bf16_lo(w.y) + e.z; a[3] = bf16_hi(w.y) + e.w;
+    } else {
+      const float4 m = *(const float4*)(src + LPTile<DT, SA_MERR_SAVE>::A_BYTES + q * LP_ESLOT + 16 * lane);
+      a[0] = m.x + e.x; a[1] = m.y + e.y; a[2] = m.z + e.z; a[3] = m.w + e.w;
+    }
+    const int row = row0 + r;
+    if (row < d.m)
+      *(float4*)(d.err_out + (int64_t)row * d.lde_out + c0 + 4 * ch) = make_float4(a[0], a[1], a[2], a[3]);
+  }
+}
+
+template <int DT, int RP, int SA, bool X3, bool TILES>
 __device__ __forceinline__ void lp_body(const Desc& d, int b,
-                                        std::conditional_t<X3, LPXSmem<RP>, LPSmem<RP>>& sm) {
+                                        std::conditional_t<X3, LPXSmem<RP>, LPSmem<RP>>& sm,
+                                        uint8_t* tiles) {
   constexpr int NU = RP / 32;               // rank tiles
   constexpr int QP = RP + 4;                // LDS pitch of a Q row (fp32 form)
   // 16-byte chunks of one K-step's Q tile per thread: fp32 form RP x 32 x 4 B,
@@ -290,28 +417,7 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b,
     }
 #pragma unroll
   for (int x = 0; x < QF4; ++x) *q_lds_ptr(0, x) = qr[0][x];
-  RawA<DT, SA, 16> ring[LP_DEPTH + 1];
-#pragma unroll
-  for (int x = 0; x <= LP_DEPTH; ++x)
-    if (x < nk) ring[x] = rawa_load<DT, SA, 16>(d, vec, row, kcol_of(c_lo, ks0, x, nk) + 16 * g, c_hi);
-  __syncthreads();
-
-  int kc = kcol_of(c_lo, ks0, 0, nk);
-  for (int it = 0; it < nk; ++it) {
-    // Q ring: slot y holds K-step it + y; fetch K-step it + LP_QAHEAD
-#pragma unroll
-    for (int y = 0; y + 1 < LP_QAHEAD; ++y)
-#pragma unroll
-      for (int x = 0; x < QF4; ++x) qr[y][x] = qr[y + 1][x];
-    if (it + LP_QAHEAD < nk) {
-      const int c = kcol_of(c_lo, ks0, it + LP_QAHEAD, nk);
-#pragma unroll
-      for (int x = 0; x < QF4; ++x) qr[LP_QAHEAD - 1][x] = *q_src_ptr(c, x);
-    }
-    float a[16];
-#pragma unroll
-    for (int j = 0; j < 16; ++j) a[j] = rawa_val<DT, SA, 16>(ring[0], j);
-    if constexpr (SA == SA_MERR_SAVE) a_store<16>(d, vec, row, kc + 16 * g, c_hi, a);
+  auto mfma_step = [&](const float a[16], int stage) {
     if constexpr (X3) {
 #pragma unroll
       for (int c = 0; c < 2; ++c) {
@@ -323,8 +429,8 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b,
           ahi[e] = h;
           alo[e] = (__bf16)(v - (float)h);
         }
-        const uint16_t* qh = &sm.q[it & 1][0][li * LB_P + 16 * g + 8 * c];
-        const uint16_t* ql = &sm.q[it & 1][1][li * LB_P + 16 * g + 8 * c];
+        const uint16_t* qh = &sm.q[stage][0][li * LB_P + 16 * g + 8 * c];
+        const uint16_t* ql = &sm.q[stage][1][li * LB_P + 16 * g + 8 * c];
 #pragma unroll
         for (int u = 0; u < NU; ++u) {
           const bf16x8 bh = *(const bf16x8*)(qh + 32 * u * LB_P);
@@ -335,7 +441,7 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b,
         }
       }
     } else {
-      const float* qb = sm.q[it & 1] + 16 * g * QP + NU * li;
+      const float* qb = sm.q[stage] + 16 * g * QP + NU * li;
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
         float bv[NU];
@@ -344,17 +450,72 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b,
         for (int u = 0; u < NU; ++u) acc[u] = mfma32(a[j], bv[u], acc[u]);
       }
     }
+  };
+  // Q ring: slot y holds K-step it + y; fetch K-step it + LP_QAHEAD
+  auto q_advance = [&](int it) {
 #pragma unroll
-    for (int x = 0; x < LP_DEPTH; ++x) ring[x] = ring[x + 1];
-    if (it + LP_DEPTH + 1 < nk)
-      ring[LP_DEPTH] = rawa_load<DT, SA, 16>(d, vec, row, kcol_of(c_lo, ks0, it + LP_DEPTH + 1, nk) + 16 * g, c_hi);
-    if (it + 1 < nk) {
-      // slot 0 now holds K-step it + 1
+    for (int y = 0; y + 1 < LP_QAHEAD; ++y)
 #pragma unroll
-      for (int x = 0; x < QF4; ++x) *q_lds_ptr((it + 1) & 1, x) = qr[0][x];
-      kc = kcol_of(c_lo, ks0, it + 1, nk);
+      for (int x = 0; x < QF4; ++x) qr[y][x] = qr[y + 1][x];
+    if (it + LP_QAHEAD < nk) {
+      const int c = kcol_of(c_lo, ks0, it + LP_QAHEAD, nk);
+#pragma unroll
+      for (int x = 0; x < QF4; ++x) qr[LP_QAHEAD - 1][x] = *q_src_ptr(c, x);
     }
+  };
+
+  // TILES: A tiles through LDS (the host picks this instance when rows are
+  // 16-byte aligned, every K-step is whole and A has a source); else A goes
+  // straight into registers.
+  if constexpr (TILES) {
+    constexpr int SB = LPTile<DT, SA>::BYTES;
+    uint8_t* const wt = tiles + wave * 2 * SB;   // this wave's two stages
+    const int wrow0 = rt * L_PROWS + 32 * wave;
+    lp_tile_issue<DT, SA>(d, wrow0, kcol_of(c_lo, ks0, 0, nk), wt);
     __syncthreads();
+    for (int it = 0; it < nk; ++it) {
+      const int kc0 = kcol_of(c_lo, ks0, it, nk);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      q_advance(it);
+      const uint8_t* cur = wt + (it & 1) * SB;
+      float a[16];
+      lp_tile_read<DT, SA>(cur, li, g, a);
+      if constexpr (SA == SA_MERR_SAVE) lp_tile_store_a<DT>(d, cur, wrow0, kc0);
+      if (it + 1 < nk) lp_tile_issue<DT, SA>(d, wrow0, kcol_of(c_lo, ks0, it + 1, nk), wt + ((it + 1) & 1) * SB);
+      mfma_step(a, it & 1);
+      if (it + 1 < nk) {
+#pragma unroll
+        for (int x = 0; x < QF4; ++x) *q_lds_ptr((it + 1) & 1, x) = qr[0][x];
+      }
+      __syncthreads();
+    }
+  } else {
+    RawA<DT, SA, 16> ring[LP_DEPTH + 1];
+#pragma unroll
+    for (int x = 0; x <= LP_DEPTH; ++x)
+      if (x < nk) ring[x] = rawa_load<DT, SA, 16>(d, vec, row, kcol_of(c_lo, ks0, x, nk) + 16 * g, c_hi);
+    __syncthreads();
+
+    int kc = kcol_of(c_lo, ks0, 0, nk);
+    for (int it = 0; it < nk; ++it) {
+      q_advance(it);
+      float a[16];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) a[j] = rawa_val<DT, SA, 16>(ring[0], j);
+      if constexpr (SA == SA_MERR_SAVE) a_store<16>(d, vec, row, kc + 16 * g, c_hi, a);
+      mfma_step(a, it & 1);
+#pragma unroll
+      for (int x = 0; x < LP_DEPTH; ++x) ring[x] = ring[x + 1];
+      if (it + LP_DEPTH + 1 < nk)
+        ring[LP_DEPTH] = rawa_load<DT, SA, 16>(d, vec, row, kcol_of(c_lo, ks0, it + LP_DEPTH + 1, nk) + 16 * g, c_hi);
+      if (it + 1 < nk) {
+        // slot 0 now holds K-step it + 1
+#pragma unroll
+        for (int x = 0; x < QF4; ++x) *q_lds_ptr((it + 1) & 1, x) = qr[0][x];
+        kc = kcol_of(c_lo, ks0, it + 1, nk);
+      }
+      __syncthreads();
+    }
   }
 
   // acc[u][v] = P[rt*128 + 32*wave + mf32_row(v, g)][NU*li + u] (this split)
@@ -371,10 +532,11 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b,
   }
 }
 
-template <int DT, int RP, int SA, bool X3>
+template <int DT, int RP, int SA, bool X3, bool TILES>
 __global__ __launch_bounds__(kBlock) void k_lp(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) std::conditional_t<X3, LPXSmem<RP>, LPSmem<RP>> sm;
-#define B_(d, b) lp_body<DT, RP, SA, X3>(d, b, sm)
+  __shared__ __attribute__((aligned(16))) uint8_t tiles[TILES ? 4 * 2 * LPTile<DT, SA>::BYTES : 16];
+#define B_(d, b) lp_body<DT, RP, SA, X3, TILES>(d, b, sm, tiles)
   OCC_DISPATCH(K_PASS_P, B_)
 #undef B_
 }
