@@ -1031,13 +1031,31 @@ __device__ __forceinline__ void la_body(const Desc& d, int b, LASmem<RP>& sm) {
     }
     if (fin) {
       // transposed: rank k, four consecutive rows per thread (rows past m
-      // carry zeros, their source rows were staged as 0)
+      // carry zeros, their source rows were staged as 0).  For bf16 M (qbf
+      // set) the right product wants the bf16 hi/lo parts of P_hat, so the
+      // same bytes hold [hi, lo][rank][m_pad] uint16 instead of fp32.
+      uint16_t* tb = d.qbf ? (uint16_t*)d.phat_t : nullptr;
       for (int idx = t; idx < RP * CR / 4; idx += kBlock) {
         const int k = idx / (CR / 4), i4 = idx % (CR / 4);
-        if (c0 + 4 * i4 < d.m_pad)
-          *(float4*)(d.phat_t + (int64_t)k * d.m_pad + c0 + 4 * i4) =
-              make_float4(sm.buf[4 * i4][k], sm.buf[4 * i4 + 1][k], sm.buf[4 * i4 + 2][k],
-                          sm.buf[4 * i4 + 3][k]);
+        if (c0 + 4 * i4 < d.m_pad) {
+          const float v[4] = {sm.buf[4 * i4][k], sm.buf[4 * i4 + 1][k], sm.buf[4 * i4 + 2][k],
+                              sm.buf[4 * i4 + 3][k]};
+          const int64_t o = (int64_t)k * d.m_pad + c0 + 4 * i4;
+          if (tb) {
+            uint16_t hi[4], lo[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const __bf16 h = (__bf16)v[e];
+              hi[e] = bf16_bits(h);
+              lo[e] = bf16_bits((__bf16)(v[e] - (float)h));
+            }
+            *(uint2*)(tb + o) = make_uint2(hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
+            *(uint2*)(tb + (int64_t)RP * d.m_pad + o) =
+                make_uint2(lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16));
+          } else {
+            *(float4*)(d.phat_t + o) = make_float4(v[0], v[1], v[2], v[3]);
+          }
+        }
       }
     }
     __syncthreads();
@@ -1178,29 +1196,34 @@ __global__ __launch_bounds__(kBlock) void k_lq(OCC_KARGS) {
 // so acc[x][u][v] = Q[col][rank 32u + mf32_row(v, g)] of this split.
 // -------------------------------------------------------------------------
 constexpr int LQX_G = 16;            // rows per group (K of two MFMA halves)
-constexpr int LQX_P = LQX_G + 8;     // LDS pitch (bf16) of a staged rank row: 48 bytes
 
+// The P_hat^T tile of a group, staged by global_load_lds_dwordx4 from the
+// bf16 hi/lo parts of the transposed P_hat (written by k_lapply): one load
+// instruction per (part, rank tile u) fills 1 KB with the 32 ranks x two
+// 8-row halves; lane l fetches rank 32u + l / 2, half (l % 2) ^ (l / 16 % 2),
+// which makes the operand reads (lane (g, li): rank 32u + li, half g)
+// conflict-free.
 template <int RP>
 struct LQXSmem {
-  uint16_t p[2][2][RP * LQX_P];      // [stage][hi, lo][rank][row]
+  uint16_t p[2][2][RP * LQX_G];      // [stage][hi, lo][rank tile][1 KB as above]
 };
+
+__device__ __forceinline__ int lqx_slot(int li, int g) { return 2 * li + (g ^ ((li >> 3) & 1)); }
 
 template <int DT, int RP, int SA>
 __device__ __forceinline__ void lqx_body(const Desc& d, int b, LQXSmem<RP>& sm) {
   constexpr int NU = RP / 32, CPL = lq_cpl(RP), BC = lq_block_cols(RP);
-  constexpr int NCH = RP * LQX_G / 4;                 // float4 chunks of a P_hat tile
-  constexpr int PFX = (NCH + kBlock - 1) / kBlock;    // per thread
-  constexpr int LQX_PAHEAD = 2;                        // P_hat groups fetched ahead
+  constexpr int NLD = 2 * NU;                         // P tile load instructions per group
   const bool vec = d.vec != 0;
   const int wave = wave_id(), lane = threadIdx.x & 63;
   const int li = lane & 31, g = lane >> 5;
-  const int t = threadIdx.x;
   const int col_tiles = (d.n + BC - 1) / BC;
   const int ct = b % col_tiles, s = b / col_tiles;
   const int cw = ct * BC + wave * 32 * CPL;
   const int col = cw + CPL * li;
   const int r_lo = s * d.q_rows, r_hi = min(d.m, r_lo + d.q_rows);
   const int ngrp = (r_hi - r_lo + LQX_G - 1) / LQX_G;
+  const uint16_t* ptb = (const uint16_t*)d.phat_t;
 
   f16v acc[CPL][NU];
 #pragma unroll
@@ -1208,40 +1231,17 @@ __device__ __forceinline__ void lqx_body(const Desc& d, int b, LQXSmem<RP>& sm) 
 #pragma unroll
     for (int u = 0; u < NU; ++u) acc[x][u] = f16v{};
 
-  // P_hat^T chunk f of group grp: rank f / 4, rows r0 + 4 (f % 4) .. + 3
-  // (zero at rows >= r_hi; phat_t rows are m_pad long and the chunks start
-  // at multiples of 4 rows, so a chunk that starts below r_hi is in bounds)
-  auto p_fetch = [&](int grp, f4v* pr) {
+  // this wave's share of the P tile loads of group grp (rows past r_hi are
+  // multiplied by the zero rows of A; the region has slack past m_pad)
+  auto p_issue = [&](int grp, int stage) {
     const int r0 = r_lo + LQX_G * grp;
+    const int rk = lane >> 1, h = (lane & 1) ^ ((lane >> 4) & 1);
 #pragma unroll
-    for (int x = 0; x < PFX; ++x) {
-      const int f = t + kBlock * x;
-      pr[x] = f4v{0.f, 0.f, 0.f, 0.f};
-      const int row = r0 + 4 * (f % 4);
-      if (f < NCH && grp < ngrp && row < r_hi) {
-        pr[x] = *(const f4v*)(d.phat_t + (int64_t)(f / 4) * d.m_pad + row);
-#pragma unroll
-        for (int e = 1; e < 4; ++e)
-          if (row + e >= r_hi) pr[x][e] = 0.f;
-      }
-    }
-  };
-  auto p_stage = [&](int stage, const f4v* pr) {
-#pragma unroll
-    for (int x = 0; x < PFX; ++x) {
-      const int f = t + kBlock * x;
-      if (f < NCH) {
-        uint16_t hi[4], lo[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const __bf16 h = (__bf16)pr[x][e];
-          hi[e] = bf16_bits(h);
-          lo[e] = bf16_bits((__bf16)(pr[x][e] - (float)h));
-        }
-        const int off = (f / 4) * LQX_P + 4 * (f % 4);
-        *(uint2*)(&sm.p[stage][0][off]) = make_uint2(hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
-        *(uint2*)(&sm.p[stage][1][off]) = make_uint2(lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16));
-      }
+    for (int j = wave; j < NLD; j += kBlock / kWave) {
+      const int part = j / NU, u = j % NU;
+      const uint16_t* src = ptb + ((int64_t)part * RP + 32 * u + rk) * d.m_pad + r0 + 8 * h;
+      __builtin_amdgcn_global_load_lds((gvoid_t*)src, (lvoid_t*)(&sm.p[stage][part][32 * u * LQX_G]),
+                                       16, 0, 0);
     }
   };
   auto a_fetch = [&](int grp, RawA<DT, SA, CPL>* x) {
@@ -1253,54 +1253,51 @@ __device__ __forceinline__ void lqx_body(const Desc& d, int b, LQXSmem<RP>& sm) 
     }
   };
 
-  // A groups are fetched LQX_ADEPTH groups ahead (a register ring), P_hat
-  // chunks LQX_PAHEAD groups ahead and staged in LDS one group ahead.
-  constexpr int LQX_ADEPTH = CPL >= 4 ? 1 : 2;   // 1 and 4 measured slower at rank 128
-  f4v pr[LQX_PAHEAD][PFX];
-#pragma unroll
-  for (int y = 0; y < LQX_PAHEAD; ++y) p_fetch(y, pr[y]);
-  p_stage(0, pr[0]);
-  RawA<DT, SA, CPL> ring[LQX_ADEPTH + 1][8];
-#pragma unroll
-  for (int y = 0; y <= LQX_ADEPTH; ++y)
-    if (y < ngrp) a_fetch(y, ring[y]);
+  RawA<DT, SA, CPL> cur[8], nxt[8];
+  if (ngrp > 0) {
+    p_issue(0, 0);
+    a_fetch(0, cur);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 
+  const int so = lqx_slot(li, g) * 8;   // this lane's operand, in bf16 elements
   for (int grp = 0; grp < ngrp; ++grp) {
     const bool more = grp + 1 < ngrp;
+    // operands of this group first, then the next group's loads
+    bf16x8 ah[NU], al[NU];
 #pragma unroll
-    for (int y = 0; y + 1 < LQX_PAHEAD; ++y)
-#pragma unroll
-      for (int x = 0; x < PFX; ++x) pr[y][x] = pr[y + 1][x];
-    p_fetch(grp + LQX_PAHEAD, pr[LQX_PAHEAD - 1]);
-    const uint16_t* ph = &sm.p[grp & 1][0][li * LQX_P + 8 * g];
-    const uint16_t* pl = &sm.p[grp & 1][1][li * LQX_P + 8 * g];
+    for (int u = 0; u < NU; ++u) {
+      ah[u] = *(const bf16x8*)(&sm.p[grp & 1][0][32 * u * LQX_G + so]);
+      al[u] = *(const bf16x8*)(&sm.p[grp & 1][1][32 * u * LQX_G + so]);
+    }
+    if (more) {
+      a_fetch(grp + 1, nxt);
+      p_issue(grp + 1, (grp + 1) & 1);
+    }
 #pragma unroll
     for (int x = 0; x < CPL; ++x) {
       bf16x8 bh, bl;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float v = rawa_val<DT, SA, CPL>(ring[0][e], x);
-        const __bf16 h = (__bf16)v;
-        bh[e] = h;
-        bl[e] = (__bf16)(v - (float)h);
+        const float v = rawa_val<DT, SA, CPL>(cur[e], x);
+        const __bf16 hv = (__bf16)v;
+        bh[e] = hv;
+        bl[e] = (__bf16)(v - (float)hv);
       }
 #pragma unroll
       for (int u = 0; u < NU; ++u) {
-        const bf16x8 ah = *(const bf16x8*)(ph + 32 * u * LQX_P);
-        const bf16x8 al = *(const bf16x8*)(pl + 32 * u * LQX_P);
-        acc[x][u] = mfma32bf(ah, bh, acc[x][u]);
-        acc[x][u] = mfma32bf(ah, bl, acc[x][u]);
-        acc[x][u] = mfma32bf(al, bh, acc[x][u]);
+        acc[x][u] = mfma32bf(ah[u], bh, acc[x][u]);
+        acc[x][u] = mfma32bf(ah[u], bl, acc[x][u]);
+        acc[x][u] = mfma32bf(al[u], bh, acc[x][u]);
       }
     }
+    // the next group's A and P tile are in before anyone reads them
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    if (more) {
 #pragma unroll
-    for (int y = 0; y < LQX_ADEPTH; ++y)
-#pragma unroll
-      for (int e = 0; e < 8; ++e) ring[y][e] = ring[y + 1][e];
-    if (grp + LQX_ADEPTH + 1 < ngrp) a_fetch(grp + LQX_ADEPTH + 1, ring[LQX_ADEPTH]);
-    // slot 0 now holds group grp + 1
-    if (more) p_stage((grp + 1) & 1, pr[0]);
+      for (int e = 0; e < 8; ++e) cur[e] = nxt[e];
+    }
     __syncthreads();
   }
 
