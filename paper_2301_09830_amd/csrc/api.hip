@@ -176,7 +176,7 @@ Slots device_slots_for(int dev) {
   bool ok = hipOccupancyMaxActiveBlocksPerMultiprocessor(
                  &bp, k_lp<DT, RP, SA_MERR_SAVE, X3, true>, kBlock, 0) == hipSuccess;
   if constexpr (X3)
-    ok = ok && hipOccupancyMaxActiveBlocksPerMultiprocessor(&bq, k_lqx<DT_F32, RP, SA_SAVED>,
+    ok = ok && hipOccupancyMaxActiveBlocksPerMultiprocessor(&bq, k_lqx<DT_F32, RP, SA_SAVED, true>,
                                                             kBlock, 0) == hipSuccess;
   else
     ok = ok && hipOccupancyMaxActiveBlocksPerMultiprocessor(&bq, k_lq<DT_F32, RP, SA_SAVED>,
@@ -454,10 +454,13 @@ occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, h
           LB("chol2", k_lchol<RP, 1>, count, LC_THREADS, flags);
           L("apply2", k_lapply<RP, 1>, b.blocks[K_APPLY]);
           if constexpr (X3) {
-            if (saved)
-              L("pass_q_a", k_lqx<DT_F32, RP, SA_SAVED>, b.blocks[K_PASS_Q]);
+            // the stored A through LDS tiles under the same conditions
+            if (saved && whole)
+              L("pass_q_a", k_lqx<DT_F32, RP, SA_SAVED, true>, b.blocks[K_PASS_Q]);
+            else if (saved)
+              L("pass_q_a", k_lqx<DT_F32, RP, SA_SAVED, false>, b.blocks[K_PASS_Q]);
             else
-              L("pass_q", k_lqx<DT, RP, SA_MERR>, b.blocks[K_PASS_Q]);
+              L("pass_q", k_lqx<DT, RP, SA_MERR, false>, b.blocks[K_PASS_Q]);
           } else {
             if (saved)
               L("pass_q_a", k_lq<DT_F32, RP, SA_SAVED>, b.blocks[K_PASS_Q]);

@@ -1032,8 +1032,9 @@ __device__ __forceinline__ void la_body(const Desc& d, int b, LASmem<RP>& sm) {
     if (fin) {
       // transposed: rank k, four consecutive rows per thread (rows past m
       // carry zeros, their source rows were staged as 0).  For bf16 M (qbf
-      // set) the right product wants the bf16 hi/lo parts of P_hat, so the
-      // same bytes hold [hi, lo][rank][m_pad] uint16 instead of fp32.
+      // set) the right product wants the bf16 hi/lo parts of P_hat in 16-row
+      // tiles, so the same bytes hold [m_pad / 16][hi, lo][rank][16] uint16
+      // instead of fp32 [rank][m_pad]: one group's tile is contiguous.
       uint16_t* tb = d.qbf ? (uint16_t*)d.phat_t : nullptr;
       for (int idx = t; idx < RP * CR / 4; idx += kBlock) {
         const int k = idx / (CR / 4), i4 = idx % (CR / 4);
@@ -1049,8 +1050,10 @@ __device__ __forceinline__ void la_body(const Desc& d, int b, LASmem<RP>& sm) {
               hi[e] = bf16_bits(h);
               lo[e] = bf16_bits((__bf16)(v[e] - (float)h));
             }
-            *(uint2*)(tb + o) = make_uint2(hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
-            *(uint2*)(tb + (int64_t)RP * d.m_pad + o) =
+            const int row = c0 + 4 * i4;
+            const int64_t ot = ((int64_t)(row >> 4) * 2 * RP + k) * 16 + (row & 15);
+            *(uint2*)(tb + ot) = make_uint2(hi[0] | ((uint32_t)hi[1] << 16), hi[2] | ((uint32_t)hi[3] << 16));
+            *(uint2*)(tb + ot + RP * 16) =
                 make_uint2(lo[0] | ((uint32_t)lo[1] << 16), lo[2] | ((uint32_t)lo[3] << 16));
           } else {
             *(float4*)(d.phat_t + o) = make_float4(v[0], v[1], v[2], v[3]);
@@ -1198,11 +1201,12 @@ __global__ __launch_bounds__(kBlock) void k_lq(OCC_KARGS) {
 constexpr int LQX_G = 16;            // rows per group (K of two MFMA halves)
 
 // The P_hat^T tile of a group, staged by global_load_lds_dwordx4 from the
-// bf16 hi/lo parts of the transposed P_hat (written by k_lapply): one load
-// instruction per (part, rank tile u) fills 1 KB with the 32 ranks x two
-// 8-row halves; lane l fetches rank 32u + l / 2, half (l % 2) ^ (l / 16 % 2),
-// which makes the operand reads (lane (g, li): rank 32u + li, half g)
-// conflict-free.
+// bf16 hi/lo parts of the transposed P_hat, which k_lapply writes in 16-row
+// tiles [m_pad / 16][hi, lo][rank][16] (groups start on 16-row boundaries):
+// one load instruction per (part, rank tile u) copies 1 KB of contiguous
+// source, the 32 ranks x two 8-row halves; lane l fetches rank 32u + l / 2,
+// half (l % 2) ^ (l / 16 % 2), which makes the operand reads (lane (g, li):
+// rank 32u + li, half g) conflict-free.
 template <int RP>
 struct LQXSmem {
   uint16_t p[2][2][RP * LQX_G];      // [stage][hi, lo][rank tile][1 KB as above]
@@ -1210,8 +1214,58 @@ struct LQXSmem {
 
 __device__ __forceinline__ int lqx_slot(int li, int g) { return 2 * li + (g ^ ((li >> 3) & 1)); }
 
-template <int DT, int RP, int SA>
-__device__ __forceinline__ void lqx_body(const Desc& d, int b, LQXSmem<RP>& sm) {
+// A tiles of the right product (TILES instances, stored fp32 A): each wave's
+// 16-row group of its 32*CPL columns comes into LDS by global_load_lds_dwordx4
+// in whole lines.  A row is 8*CPL chunks of 16 bytes; one instruction fills a
+// 1 KB slot with 8/CPL rows (lane l: row l / (8 CPL), chunk l % (8 CPL)).
+// Slots are 1152 bytes apart, so at CPL = 1 (one 128-byte row per half-wave
+// of an operand read) rows e and 8 + e fall in opposite halves of the banks.
+constexpr int LQX_SLOT = 1024 + 128;
+template <int RP>
+struct LQXTile {
+  static constexpr int CPL = lq_cpl(RP);
+  static constexpr int RPI = 8 / CPL;                 // rows per load instruction
+  static constexpr int NI = LQX_G / RPI;              // slots per group
+  static constexpr int BYTES = NI * LQX_SLOT;         // one stage of one wave
+  // stages per wave: at rank 128 the A tiles run three groups ahead (with
+  // the P tile's two stages, three blocks fit a compute unit's LDS)
+  static constexpr int AST = RP >= 128 ? 4 : 2;
+};
+
+// Rows r0 .. r0+15 (clamped to r_last) of columns cw .. cw + 32 CPL - 1
+// (chunks past the last column read the row's last chunk instead; those
+// columns are never stored).
+template <int RP>
+__device__ __forceinline__ void lqx_tile_issue(const Desc& d, int r0, int r_last, int cw, uint8_t* dst) {
+  using T = LQXTile<RP>;
+  constexpr int CH = 8 * T::CPL;
+  const int lane = threadIdx.x & 63;
+  const int rr = lane / CH, ch = lane % CH;
+  const int c = min(cw + 4 * ch, d.n - 4);
+#pragma unroll
+  for (int q = 0; q < T::NI; ++q) {
+    const int row = min(r0 + q * T::RPI + rr, r_last);
+    __builtin_amdgcn_global_load_lds((gvoid_t*)(d.err_out + (int64_t)row * d.lde_out + c),
+                                     (lvoid_t*)(dst + q * LQX_SLOT), 16, 0, 0);
+  }
+}
+
+// a[e][x] = A[row 8g + e of the group][column CPL li + x of the wave]
+template <int RP>
+__device__ __forceinline__ void lqx_tile_read(const uint8_t* src, int li, int g,
+                                              float (&a)[8][LQXTile<RP>::CPL]) {
+  using T = LQXTile<RP>;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int r = 8 * g + e;
+    const float* p = (const float*)(src + (r / T::RPI) * LQX_SLOT + (r % T::RPI) * (128 * T::CPL)) +
+                     T::CPL * li;
+    ld_f<T::CPL>(p, a[e]);
+  }
+}
+
+template <int DT, int RP, int SA, bool TILES>
+__device__ __forceinline__ void lqx_body(const Desc& d, int b, LQXSmem<RP>& sm, uint8_t* tiles) {
   constexpr int NU = RP / 32, CPL = lq_cpl(RP), BC = lq_block_cols(RP);
   constexpr int NLD = 2 * NU;                         // P tile load instructions per group
   const bool vec = d.vec != 0;
@@ -1232,14 +1286,14 @@ __device__ __forceinline__ void lqx_body(const Desc& d, int b, LQXSmem<RP>& sm) 
     for (int u = 0; u < NU; ++u) acc[x][u] = f16v{};
 
   // this wave's share of the P tile loads of group grp (rows past r_hi are
-  // multiplied by the zero rows of A; the region has slack past m_pad)
+  // multiplied by the zero rows of A)
   auto p_issue = [&](int grp, int stage) {
-    const int r0 = r_lo + LQX_G * grp;
+    const int r0 = r_lo + LQX_G * grp;   // a multiple of 16
     const int rk = lane >> 1, h = (lane & 1) ^ ((lane >> 4) & 1);
 #pragma unroll
     for (int j = wave; j < NLD; j += kBlock / kWave) {
       const int part = j / NU, u = j % NU;
-      const uint16_t* src = ptb + ((int64_t)part * RP + 32 * u + rk) * d.m_pad + r0 + 8 * h;
+      const uint16_t* src = ptb + (((int64_t)(r0 >> 4) * 2 + part) * RP + 32 * u + rk) * 16 + 8 * h;
       __builtin_amdgcn_global_load_lds((gvoid_t*)src, (lvoid_t*)(&sm.p[stage][part][32 * u * LQX_G]),
                                        16, 0, 0);
     }
@@ -1253,52 +1307,151 @@ __device__ __forceinline__ void lqx_body(const Desc& d, int b, LQXSmem<RP>& sm) 
     }
   };
 
-  RawA<DT, SA, CPL> cur[8], nxt[8];
-  if (ngrp > 0) {
-    p_issue(0, 0);
-    a_fetch(0, cur);
-  }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-
-  const int so = lqx_slot(li, g) * 8;   // this lane's operand, in bf16 elements
-  for (int grp = 0; grp < ngrp; ++grp) {
-    const bool more = grp + 1 < ngrp;
-    // operands of this group first, then the next group's loads
-    bf16x8 ah[NU], al[NU];
+  auto mfma_group = [&](const bf16x8 (&ah)[NU], const bf16x8 (&al)[NU], int x, const bf16x8& bh,
+                        const bf16x8& bl) {
 #pragma unroll
     for (int u = 0; u < NU; ++u) {
-      ah[u] = *(const bf16x8*)(&sm.p[grp & 1][0][32 * u * LQX_G + so]);
-      al[u] = *(const bf16x8*)(&sm.p[grp & 1][1][32 * u * LQX_G + so]);
+      acc[x][u] = mfma32bf(ah[u], bh, acc[x][u]);
+      acc[x][u] = mfma32bf(ah[u], bl, acc[x][u]);
+      acc[x][u] = mfma32bf(al[u], bh, acc[x][u]);
     }
-    if (more) {
-      a_fetch(grp + 1, nxt);
-      p_issue(grp + 1, (grp + 1) & 1);
-    }
+  };
+  const int so = lqx_slot(li, g) * 8;   // this lane's P operand, in bf16 elements
+
+  if constexpr (TILES) {
+    // Per group: wait for this group's A tile and P share, barrier (every
+    // wave's share of the P tile is in; every wave is done with the other P
+    // stage), read the operands, issue the next group's P share and the A
+    // tile AST - 1 groups ahead, run the products.  Loads complete in order:
+    // with AST > 2 the A tile issued after the P share this group waits for
+    // (group grp + AST - 2) may still be in flight at the wait.
+    static_assert(SA == SA_SAVED, "A tiles hold the stored fp32 A");
+    using T = LQXTile<RP>;
+    constexpr int AST = T::AST;
+    uint8_t* const wt = tiles + wave * AST * T::BYTES;
+    const int r_last = r_hi - 1;
+    if (ngrp > 0) p_issue(0, 0);
 #pragma unroll
-    for (int x = 0; x < CPL; ++x) {
-      bf16x8 bh, bl;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float v = rawa_val<DT, SA, CPL>(cur[e], x);
-        const __bf16 hv = (__bf16)v;
-        bh[e] = hv;
-        bl[e] = (__bf16)(v - (float)hv);
+    for (int y = 0; y + 1 < AST; ++y)
+      if (y < ngrp) lqx_tile_issue<RP>(d, r_lo + LQX_G * y, r_last, cw, wt + y * T::BYTES);
+    int st_cur = 0;                         // A stage of group grp
+    for (int grp = 0; grp < ngrp; ++grp) {
+      const int r0 = r_lo + LQX_G * grp;
+      if (AST > 2 && grp > 0 && grp + AST - 2 < ngrp) {
+        static_assert(T::NI <= 15, "vmcnt immediate");
+        asm volatile("s_waitcnt vmcnt(%0)" :: "n"(T::NI) : "memory");
+      } else {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       }
+      // A bare barrier: every wave has waited for its own share above and
+      // has consumed its earlier LDS reads, and a fence here would wait for
+      // the A tile still in flight.
+      asm volatile("s_barrier" ::: "memory");
+      bf16x8 ah[NU], al[NU];
+      float av[8][CPL];
+      if constexpr (AST > 2) {
+        // The operand reads as inline assembly: the compiler cannot tell that
+        // the A tile in flight targets another stage and would wait for it
+        // before any LDS read.
+        static_assert(NU == 4 && CPL == 1, "assembly reads are written for rank 128");
+        const uint32_t pa = (uint32_t)(size_t)(lvoid_t*)(&sm.p[grp & 1][0][so]);
+        const uint32_t aa = (uint32_t)(size_t)(lvoid_t*)(wt + st_cur * T::BYTES + g * LQX_SLOT + 4 * li);
+        constexpr int PB = RP * LQX_G * 2;   // bytes of one part (hi or lo) of a P stage
+        constexpr int UB = 32 * LQX_G * 2;   // bytes of one rank tile of a part
+        asm volatile(
+            "ds_read_b128 %0, %16 offset:%18\n\t"
+            "ds_read_b128 %1, %16 offset:%19\n\t"
+            "ds_read_b128 %2, %16 offset:%20\n\t"
+            "ds_read_b128 %3, %16 offset:%21\n\t"
+            "ds_read_b128 %4, %16 offset:%22\n\t"
+            "ds_read_b128 %5, %16 offset:%23\n\t"
+            "ds_read_b128 %6, %16 offset:%24\n\t"
+            "ds_read_b128 %7, %16 offset:%25\n\t"
+            "ds_read_b32 %8, %17 offset:0\n\t"
+            "ds_read_b32 %9, %17 offset:128\n\t"
+            "ds_read_b32 %10, %17 offset:256\n\t"
+            "ds_read_b32 %11, %17 offset:384\n\t"
+            "ds_read_b32 %12, %17 offset:512\n\t"
+            "ds_read_b32 %13, %17 offset:640\n\t"
+            "ds_read_b32 %14, %17 offset:768\n\t"
+            "ds_read_b32 %15, %17 offset:896\n\t"
+            "s_waitcnt lgkmcnt(0)"
+            : "=&v"(ah[0]), "=&v"(ah[1]), "=&v"(ah[2]), "=&v"(ah[3]),
+              "=&v"(al[0]), "=&v"(al[1]), "=&v"(al[2]), "=&v"(al[3]),
+              "=&v"(av[0][0]), "=&v"(av[1][0]), "=&v"(av[2][0]), "=&v"(av[3][0]),
+              "=&v"(av[4][0]), "=&v"(av[5][0]), "=&v"(av[6][0]), "=&v"(av[7][0])
+            : "v"(pa), "v"(aa), "n"(0), "n"(UB), "n"(2 * UB), "n"(3 * UB),
+              "n"(PB), "n"(PB + UB), "n"(PB + 2 * UB), "n"(PB + 3 * UB)
+            : "memory");
+      } else {
+#pragma unroll
+        for (int u = 0; u < NU; ++u) {
+          ah[u] = *(const bf16x8*)(&sm.p[grp & 1][0][32 * u * LQX_G + so]);
+          al[u] = *(const bf16x8*)(&sm.p[grp & 1][1][32 * u * LQX_G + so]);
+        }
+        lqx_tile_read<RP>(wt + st_cur * T::BYTES, li, g, av);
+      }
+      const int st_new = st_cur == 0 ? AST - 1 : st_cur - 1;   // stage of group grp + AST - 1
+      if (grp + 1 < ngrp) p_issue(grp + 1, (grp + 1) & 1);
+      if (grp + AST - 1 < ngrp)
+        lqx_tile_issue<RP>(d, r0 + LQX_G * (AST - 1), r_last, cw, wt + st_new * T::BYTES);
+      st_cur = st_cur + 1 == AST ? 0 : st_cur + 1;
+      const int nvalid = r_hi - r0 - 8 * g;   // rows of this lane's half inside the split
+#pragma unroll
+      for (int x = 0; x < CPL; ++x) {
+        bf16x8 bh, bl;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float v = e < nvalid ? av[e][x] : 0.f;
+          const __bf16 hv = (__bf16)v;
+          bh[e] = hv;
+          bl[e] = (__bf16)(v - (float)hv);
+        }
+        mfma_group(ah, al, x, bh, bl);
+      }
+    }
+  } else {
+    RawA<DT, SA, CPL> cur[8], nxt[8];
+    if (ngrp > 0) {
+      p_issue(0, 0);
+      a_fetch(0, cur);
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+
+    for (int grp = 0; grp < ngrp; ++grp) {
+      const bool more = grp + 1 < ngrp;
+      // operands of this group first, then the next group's loads
+      bf16x8 ah[NU], al[NU];
 #pragma unroll
       for (int u = 0; u < NU; ++u) {
-        acc[x][u] = mfma32bf(ah[u], bh, acc[x][u]);
-        acc[x][u] = mfma32bf(ah[u], bl, acc[x][u]);
-        acc[x][u] = mfma32bf(al[u], bh, acc[x][u]);
+        ah[u] = *(const bf16x8*)(&sm.p[grp & 1][0][32 * u * LQX_G + so]);
+        al[u] = *(const bf16x8*)(&sm.p[grp & 1][1][32 * u * LQX_G + so]);
       }
-    }
-    // the next group's A and P tile are in before anyone reads them
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    if (more) {
+      if (more) {
+        a_fetch(grp + 1, nxt);
+        p_issue(grp + 1, (grp + 1) & 1);
+      }
 #pragma unroll
-      for (int e = 0; e < 8; ++e) cur[e] = nxt[e];
+      for (int x = 0; x < CPL; ++x) {
+        bf16x8 bh, bl;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float v = rawa_val<DT, SA, CPL>(cur[e], x);
+          const __bf16 hv = (__bf16)v;
+          bh[e] = hv;
+          bl[e] = (__bf16)(v - (float)hv);
+        }
+        mfma_group(ah, al, x, bh, bl);
+      }
+      // the next group's A and P tile are in before anyone reads them
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      if (more) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) cur[e] = nxt[e];
+      }
+      __syncthreads();
     }
-    __syncthreads();
   }
 
   // acc[x][u][4q + w] = Q[col + x][rank 32u + 8q + 4g + w] (this split)
@@ -1317,10 +1470,11 @@ __device__ __forceinline__ void lqx_body(const Desc& d, int b, LQXSmem<RP>& sm) 
   }
 }
 
-template <int DT, int RP, int SA>
+template <int DT, int RP, int SA, bool TILES>
 __global__ __launch_bounds__(kBlock) void k_lqx(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) LQXSmem<RP> sm;
-#define B_(d, b) lqx_body<DT, RP, SA>(d, b, sm)
+  __shared__ __attribute__((aligned(16))) uint8_t tiles[TILES ? 4 * LQXTile<RP>::AST * LQXTile<RP>::BYTES : 16];
+#define B_(d, b) lqx_body<DT, RP, SA, TILES>(d, b, sm, tiles)
   OCC_DISPATCH(K_PASS_Q, B_)
 #undef B_
 }

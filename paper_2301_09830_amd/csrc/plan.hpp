@@ -181,7 +181,9 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0,
   // right product: column tiles, rows split
   const int64_t ctq = cdiv(n, lq_block_cols(rp));
   const int64_t sq = clamp64(cdiv(target_q, ctq), 1, cdiv(m, L_MIN_ROWS));
-  t.q_rows = (int)round_up(cdiv(m, sq), L_QG);
+  // splits start on 16-row boundaries: the bf16 right product walks 16-row
+  // groups, and its P_hat^T parts are stored in 16-row tiles
+  t.q_rows = (int)round_up(cdiv(m, sq), 2 * L_QG);
   t.sq = (int)cdiv(m, t.q_rows);
   // reconstruction: column tiles x row blocks (multiple of 32 rows)
   const int64_t ctm = cdiv(n, lm_block_cols(rp));
@@ -226,7 +228,7 @@ inline Regions matrix_regions(int64_t m, int64_t n, int rp, const Tiling& t) {
   g.info = take(64);
   // + 64 bytes: the right product's tile loads may run up to 8 rows past
   // m_pad in the last rank row
-  g.phat_t = take(rp > kFusedMaxRank ? (size_t)rp * t.m_pad * 4 + 64 : 0);
+  g.phat_t = take(rp > kFusedMaxRank ? (size_t)rp * t.m_pad * 4 : 0);
   g.qbf = take(rp > kFusedMaxRank ? (size_t)2 * rp * t.n_pad * 2 : 0);
   g.total = off;
   return g;

@@ -58,6 +58,24 @@ def test_bf16_whole_ksteps_lds_tiles(shape, rank):
     assert_parity(res, "bf16", f"bf16 {shape[0]}x{shape[1]} r{rank} (LDS tiles)")
 
 
+@pytest.mark.parametrize("shape,rank", [(s, r) for r in (32, 64, 128)
+                                        for s in ((1000, 512), (4100, 224), (130, 128), (300, 160))]
+                         + [((77, 32), 32), ((77, 96), 64)])
+def test_bf16_large_rank_whole_columns(shape, rank):
+    """bf16 M at rank > 16 whose width is a multiple of 32 columns: the left
+    products and the right product stage the stored A through LDS tiles, the
+    right product its P_hat^T operand from 16-row tiles.  Covers several row
+    splits with a ragged last group (4100 rows), a single ragged group (77),
+    waves whose columns run past n (96, 160 and 224 columns at ranks 32 and
+    64) and waves wholly past n (160 and 224 columns at rank 128).  The bound
+    is the split-product accuracy bound of the test below."""
+    w = WORKLOADS[5].scaled([shape], rank=rank, signal_rank=160)
+    res, _, _ = run_workload(w, 2)
+    assert_parity(res, "bf16", f"bf16 {shape[0]}x{shape[1]} r{rank} (LDS tiles)")
+    worst = max(max(r["mhat"], r["err"]) for step in res for r in step)
+    assert worst <= 5e-4, f"split products off: {worst:.3e}"
+
+
 def test_config3_stage_batched_small():
     shapes = [(3 * 96, 96), (96, 96), (4 * 96, 96), (96, 4 * 96)] * 2
     w = WORKLOADS[3].scaled(shapes)
