@@ -179,7 +179,7 @@ Slots device_slots_for(int dev) {
     ok = ok && hipOccupancyMaxActiveBlocksPerMultiprocessor(&bq, k_lqx<DT_F32, RP, SA_SAVED, true>,
                                                             kBlock, 0) == hipSuccess;
   else
-    ok = ok && hipOccupancyMaxActiveBlocksPerMultiprocessor(&bq, k_lq<DT_F32, RP, SA_SAVED>,
+    ok = ok && hipOccupancyMaxActiveBlocksPerMultiprocessor(&bq, k_lq<DT_F32, RP, SA_SAVED, true>,
                                                             kBlock, 0) == hipSuccess;
   if constexpr (X3)
     ok = ok && hipOccupancyMaxActiveBlocksPerMultiprocessor(&bm, k_mlx<RP, 0, true, true>, kBlock,
@@ -462,10 +462,12 @@ occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, h
             else
               L("pass_q", k_lqx<DT, RP, SA_MERR, false>, b.blocks[K_PASS_Q]);
           } else {
-            if (saved)
-              L("pass_q_a", k_lq<DT_F32, RP, SA_SAVED>, b.blocks[K_PASS_Q]);
+            if (saved && whole)
+              L("pass_q_a", k_lq<DT_F32, RP, SA_SAVED, true>, b.blocks[K_PASS_Q]);
+            else if (saved)
+              L("pass_q_a", k_lq<DT_F32, RP, SA_SAVED, false>, b.blocks[K_PASS_Q]);
             else
-              L("pass_q", k_lq<DT, RP, SA_MERR>, b.blocks[K_PASS_Q]);
+              L("pass_q", k_lq<DT, RP, SA_MERR, false>, b.blocks[K_PASS_Q]);
           }
           L("q_reduce", k_qredl<RP>, b.blocks[K_QRED]);
         }

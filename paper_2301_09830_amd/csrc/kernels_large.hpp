@@ -1178,12 +1178,170 @@ __device__ __forceinline__ void lq_body(const Desc& d, int b, LQSmem<RP>& sm) {
     }
 }
 
-template <int DT, int RP, int SA>
+// TILES form of k_lq for the stored fp32 A (rows 16-byte aligned, n a
+// multiple of 32): both operands of a group come into LDS by DMA, AST - 1
+// groups ahead, so the loads in flight are not bounded by registers.
+//   A: each wave's 8 rows x 32 CPL columns, 8/CPL rows per 1 KB
+//      global_load_lds_dwordx4 (lane l: row l / (8 CPL), chunk l % (8 CPL));
+//      rows are contiguous in LDS, so the operand reads (lane (g, li): CPL
+//      floats of row 2ks + g at column CPL li) are conflict-free;
+//   P: the block's 8 rows x RP of P_hat (contiguous in memory), each wave
+//      copying RP/32 runs of 256 bytes with global_load_lds_dword.
+// Every wave issues the same number of loads per group, so one wait count
+// covers the groups still in flight; the operand reads are inline ds_read
+// instructions (the compiler would wait for every DMA in flight before a
+// plain LDS read).
+template <int RP>
+struct LQTile {
+  static constexpr int CPL = lq_cpl(RP), NU = RP / 32;
+  static constexpr int NI = CPL;                       // A loads per wave and group
+  static constexpr int NP = RP / 32;                   // P loads per wave and group
+  static constexpr int A_BYTES = 1024 * CPL;           // one wave's A tile
+  static constexpr int P_BYTES = L_QG * RP * 4;        // the block's P tile
+  static constexpr int STAGE = 4 * A_BYTES + P_BYTES;
+  static constexpr int AST = RP >= 128 ? 4 : 3;        // stages (3 blocks per CU at rank 32)
+};
+
+template <int W> struct LdsVec;
+template <> struct LdsVec<1> { typedef float T; };
+template <> struct LdsVec<2> { typedef float T __attribute__((ext_vector_type(2))); };
+template <> struct LdsVec<4> { typedef f4v T; };
+
+template <int W>
+__device__ __forceinline__ void ds_read_asm(typename LdsVec<W>::T& v, uint32_t addr) {
+  if constexpr (W == 1) asm volatile("ds_read_b32 %0, %1" : "=v"(v) : "v"(addr) : "memory");
+  else if constexpr (W == 2) asm volatile("ds_read_b64 %0, %1" : "=v"(v) : "v"(addr) : "memory");
+  else asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr) : "memory");
+}
+
+template <int W>
+__device__ __forceinline__ float lds_elem(const typename LdsVec<W>::T& v, int j) {
+  if constexpr (W == 1) return v;
+  else return v[j];
+}
+
+template <int RP>
+__device__ __forceinline__ void lq_tile_issue(const Desc& d, int r0, int r_last, int cw, int wave,
+                                              uint8_t* stage) {
+  using T = LQTile<RP>;
+  constexpr int CH = 8 * T::CPL, RPI = 8 / T::CPL;
+  const int lane = threadIdx.x & 63;
+  const int rr = lane / CH, ch = lane % CH;
+  const int c = min(cw + 4 * ch, d.n - 4);
+  uint8_t* adst = stage + wave * T::A_BYTES;
+#pragma unroll
+  for (int q = 0; q < T::NI; ++q) {
+    const int row = min(r0 + q * RPI + rr, r_last);
+    __builtin_amdgcn_global_load_lds((gvoid_t*)(d.err_out + (int64_t)row * d.lde_out + c),
+                                     (lvoid_t*)(adst + q * 1024), 16, 0, 0);
+  }
+  uint8_t* pdst = stage + 4 * T::A_BYTES;
+#pragma unroll
+  for (int j = 0; j < T::NP; ++j) {
+    const int run = wave * T::NP + j;                  // 64-float run of the P tile
+    const int idx = run * 64 + lane;
+    const int row = min(r0 + idx / RP, d.m - 1);        // rows past m: any finite value
+    __builtin_amdgcn_global_load_lds((gvoid_t*)(d.phat + (int64_t)row * RP + idx % RP),
+                                     (lvoid_t*)(pdst + run * 256), 4, 0, 0);
+  }
+}
+
+template <int RP>
+__device__ __forceinline__ void lq_tiles_body(const Desc& d, int b, uint8_t* tiles) {
+  using T = LQTile<RP>;
+  constexpr int NU = T::NU, CPL = T::CPL, BC = lq_block_cols(RP), AST = T::AST;
+  constexpr int PER_GROUP = T::NI + T::NP;
+  const int wave = wave_id(), lane = threadIdx.x & 63;
+  const int li = lane & 31, g = lane >> 5;
+  const int col_tiles = (d.n + BC - 1) / BC;
+  const int ct = b % col_tiles, s = b / col_tiles;
+  const int cw = ct * BC + wave * 32 * CPL;
+  const int col = cw + CPL * li;
+  const int r_lo = s * d.q_rows, r_hi = min(d.m, r_lo + d.q_rows);
+  const int ngrp = (r_hi - r_lo + L_QG - 1) / L_QG;
+  const int r_last = r_hi - 1;
+
+  f16v acc[CPL][NU];
+#pragma unroll
+  for (int x = 0; x < CPL; ++x)
+#pragma unroll
+    for (int u = 0; u < NU; ++u) acc[x][u] = f16v{};
+
+#pragma unroll
+  for (int y = 0; y + 1 < AST; ++y)
+    if (y < ngrp) lq_tile_issue<RP>(d, r_lo + L_QG * y, r_last, cw, wave, tiles + y * T::STAGE);
+
+  const uint32_t tbase = (uint32_t)(size_t)(lvoid_t*)tiles;
+  int st_cur = 0;
+  for (int grp = 0; grp < ngrp; ++grp) {
+    const int r0 = r_lo + L_QG * grp;
+    // groups issued after this one and possibly still in flight
+    const int after = min(grp + AST - 2, ngrp - 1) - grp;
+    static_assert(AST <= 4 && 2 * PER_GROUP <= 63, "vmcnt immediates");
+    if (after <= 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    else if (after == 1) asm volatile("s_waitcnt vmcnt(%0)" :: "n"(PER_GROUP) : "memory");
+    else asm volatile("s_waitcnt vmcnt(%0)" :: "n"(2 * PER_GROUP) : "memory");
+    asm volatile("s_barrier" ::: "memory");   // every wave's P share is in
+
+    typename LdsVec<CPL>::T av[4];
+    typename LdsVec<NU>::T pv[4];
+    const uint32_t sb = tbase + st_cur * T::STAGE;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const int r = 2 * ks + g;
+      ds_read_asm<CPL>(av[ks], sb + wave * T::A_BYTES + r * 128 * CPL + 4 * CPL * li);
+      ds_read_asm<NU>(pv[ks], sb + 4 * T::A_BYTES + (r * RP + NU * li) * 4);
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)"
+                 : "+v"(av[0]), "+v"(av[1]), "+v"(av[2]), "+v"(av[3]),
+                   "+v"(pv[0]), "+v"(pv[1]), "+v"(pv[2]), "+v"(pv[3]));
+
+    const int st_new = st_cur == 0 ? AST - 1 : st_cur - 1;   // stage of group grp + AST - 1
+    if (grp + AST - 1 < ngrp)
+      lq_tile_issue<RP>(d, r0 + L_QG * (AST - 1), r_last, cw, wave, tiles + st_new * T::STAGE);
+    st_cur = st_cur + 1 == AST ? 0 : st_cur + 1;
+
+    const int nvalid = r_hi - r0 - g;   // rows 2ks + g of this group inside the split: 2ks < nvalid
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+#pragma unroll
+      for (int x = 0; x < CPL; ++x) {
+        const float a = 2 * ks < nvalid ? lds_elem<CPL>(av[ks], x) : 0.f;
+#pragma unroll
+        for (int u = 0; u < NU; ++u) acc[x][u] = mfma32(a, lds_elem<NU>(pv[ks], u), acc[x][u]);
+      }
+    }
+  }
+
+#pragma unroll
+  for (int x = 0; x < CPL; ++x)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int c = cw + CPL * mf32_row(v, g) + x;
+      if (c < d.n) {
+        float o[NU];
+#pragma unroll
+        for (int u = 0; u < NU; ++u) o[u] = acc[x][u][v];
+        st_f<NU>(d.qpart + ((int64_t)s * d.n + c) * RP + NU * li, o);
+      }
+    }
+  (void)col;
+}
+
+template <int DT, int RP, int SA, bool TILES>
 __global__ __launch_bounds__(kBlock) void k_lq(OCC_KARGS) {
-  __shared__ __attribute__((aligned(16))) LQSmem<RP> sm;
-#define B_(d, b) lq_body<DT, RP, SA>(d, b, sm)
-  OCC_DISPATCH(K_PASS_Q, B_)
+  if constexpr (TILES) {
+    static_assert(DT == DT_F32 && SA == SA_SAVED, "tiles hold the stored fp32 A");
+    __shared__ __attribute__((aligned(16))) uint8_t tiles[LQTile<RP>::AST * LQTile<RP>::STAGE];
+#define B_(d, b) lq_tiles_body<RP>(d, b, tiles)
+    OCC_DISPATCH(K_PASS_Q, B_)
 #undef B_
+  } else {
+    __shared__ __attribute__((aligned(16))) LQSmem<RP> sm;
+#define B_(d, b) lq_body<DT, RP, SA>(d, b, sm)
+    OCC_DISPATCH(K_PASS_Q, B_)
+#undef B_
+  }
 }
 
 // -------------------------------------------------------------------------

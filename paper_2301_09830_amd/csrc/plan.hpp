@@ -226,8 +226,6 @@ inline Regions matrix_regions(int64_t m, int64_t n, int rp, const Tiling& t) {
   g.t1 = take((size_t)rp * rp * 8);
   g.tm = take((size_t)rp * rp * 8);
   g.info = take(64);
-  // + 64 bytes: the right product's tile loads may run up to 8 rows past
-  // m_pad in the last rank row
   g.phat_t = take(rp > kFusedMaxRank ? (size_t)rp * t.m_pad * 4 : 0);
   g.qbf = take(rp > kFusedMaxRank ? (size_t)2 * rp * t.n_pad * 2 : 0);
   g.total = off;

@@ -76,6 +76,19 @@ def test_bf16_large_rank_whole_columns(shape, rank):
     assert worst <= 5e-4, f"split products off: {worst:.3e}"
 
 
+@pytest.mark.parametrize("shape,rank", [(s, r) for r in (32, 64, 128)
+                                        for s in ((1000, 512), (4100, 224), (130, 128), (300, 160))]
+                         + [((77, 32), 32), ((77, 96), 64)])
+def test_fp32_large_rank_whole_columns(shape, rank):
+    """fp32 M at rank > 16 whose width is a multiple of 32 columns: the left
+    products stage A through LDS tiles and the right product stages the
+    stored A and the P_hat rows by DMA several groups ahead.  The same edge
+    cases as the bf16 test above (ragged last groups, waves past n)."""
+    w = WORKLOADS[3].scaled([shape], rank=rank)
+    res, _, _ = run_workload(w, 2)
+    assert_parity(res, "f32", f"fp32 {shape[0]}x{shape[1]} r{rank} (LDS tiles)")
+
+
 def test_config3_stage_batched_small():
     shapes = [(3 * 96, 96), (96, 96), (4 * 96, 96), (96, 4 * 96)] * 2
     w = WORKLOADS[3].scaled(shapes)

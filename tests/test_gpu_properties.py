@@ -110,22 +110,23 @@ def test_compress_without_error_buffer(rank, n):
     assert torch.equal(Pa, Pb) and torch.equal(Qa, Qb)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("rank", [32, 64, 128])
-def test_large_rank_tile_paths_match_scalar_paths(rank):
-    """bf16 M, rank > 16, 224 columns: with 16-byte aligned rows the left and
-    right products take their LDS-tile paths; with a leading dimension of
-    n + 1 every pass takes its scalar path.  The products see the same
-    operands in the same order, so the two runs agree bit for bit."""
+def test_large_rank_tile_paths_match_scalar_paths(rank, dtype):
+    """Rank > 16, 224 columns: with 16-byte aligned rows the left and right
+    products take their LDS-tile paths; with a leading dimension of n + 1
+    every pass takes its scalar path.  The products see the same operands in
+    the same order, so the two runs agree bit for bit."""
     from paper_2301_09830_amd import optcc
     torch = torch_mod()
     m, n = 1000, 224
-    w, M, q0 = _inputs(m=m, n=n, rank=rank)
+    w, M, q0 = _inputs(m=m, n=n, rank=rank, dtype=dtype)
     e0 = np.random.default_rng(7).standard_normal((m, n)).astype(np.float32) * 1e-2
     out = []
     for pad in (0, 1):
         full = np.zeros((m, n + pad), dtype=M.dtype)
         full[:, :n] = M
-        Md = to_device(full, "bf16")[:, :n]
+        Md = to_device(full, dtype)[:, :n]
         err_full = torch.zeros((m, n + pad), device="cuda")
         err = err_full[:, :n]
         err.copy_(torch.from_numpy(e0).cuda())
@@ -136,7 +137,7 @@ def test_large_rank_tile_paths_match_scalar_paths(rank):
         torch.cuda.synchronize()
         out.append((P, Q, Mh_full[:, :n].contiguous(), err.contiguous()))
     for a, b, name in zip(out[0], out[1], ("P", "Q", "M_hat", "err")):
-        assert torch.equal(a, b), f"rank {rank}: {name} differs between the tile and scalar paths"
+        assert torch.equal(a, b), f"{dtype} rank {rank}: {name} differs between the tile and scalar paths"
 
 
 @pytest.mark.parametrize("rank", [16, 48])
