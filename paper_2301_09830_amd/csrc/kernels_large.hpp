@@ -1202,24 +1202,6 @@ struct LQTile {
   static constexpr int AST = RP >= 128 ? 4 : 3;        // stages (3 blocks per CU at rank 32)
 };
 
-template <int W> struct LdsVec;
-template <> struct LdsVec<1> { typedef float T; };
-template <> struct LdsVec<2> { typedef float T __attribute__((ext_vector_type(2))); };
-template <> struct LdsVec<4> { typedef f4v T; };
-
-template <int W>
-__device__ __forceinline__ void ds_read_asm(typename LdsVec<W>::T& v, uint32_t addr) {
-  if constexpr (W == 1) asm volatile("ds_read_b32 %0, %1" : "=v"(v) : "v"(addr) : "memory");
-  else if constexpr (W == 2) asm volatile("ds_read_b64 %0, %1" : "=v"(v) : "v"(addr) : "memory");
-  else asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr) : "memory");
-}
-
-template <int W>
-__device__ __forceinline__ float lds_elem(const typename LdsVec<W>::T& v, int j) {
-  if constexpr (W == 1) return v;
-  else return v[j];
-}
-
 template <int RP>
 __device__ __forceinline__ void lq_tile_issue(const Desc& d, int r0, int r_last, int cw, int wave,
                                               uint8_t* stage) {

@@ -32,9 +32,32 @@ namespace occ {
 
 typedef float f4v __attribute__((ext_vector_type(4)));
 
+// LDS reads of W floats issued as inline assembly, for loops with LDS DMA of
+// other stages still in flight (the compiler cannot tell those apart from the
+// stage being read and would wait for them).  The caller ends a batch of them
+// with s_waitcnt lgkmcnt(0), taking the read values as "+v" operands so that
+// no use moves above the wait.
+template <int W> struct LdsVec;
+template <> struct LdsVec<1> { typedef float T; };
+template <> struct LdsVec<2> { typedef float T __attribute__((ext_vector_type(2))); };
+template <> struct LdsVec<4> { typedef f4v T; };
+
+template <int W>
+__device__ __forceinline__ void ds_read_asm(typename LdsVec<W>::T& v, uint32_t addr) {
+  if constexpr (W == 1) asm volatile("ds_read_b32 %0, %1" : "=v"(v) : "v"(addr) : "memory");
+  else if constexpr (W == 2) asm volatile("ds_read_b64 %0, %1" : "=v"(v) : "v"(addr) : "memory");
+  else asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr) : "memory");
+}
+
+template <int W>
+__device__ __forceinline__ float lds_elem(const typename LdsVec<W>::T& v, int j) {
+  if constexpr (W == 1) return v;
+  else return v[j];
+}
+
 constexpr int PM_RB = 2;                  // 16-row MFMA tiles per block in k_pm
 constexpr int PM_ROWS = 16 * PM_RB;       // rows per block (== F_PROWS)
-constexpr int PM_WAVES = 8;               // waves per block in k_pm
+constexpr int PM_WAVES = 4;               // waves per block in k_pm
 constexpr int PM_THREADS = PM_WAVES * kWave;
 static_assert(PM_ROWS == F_PROWS, "k_pm block rows must match the plan");
 constexpr int QM_COLS = F_QCOLS;          // columns per block in k_qm
@@ -121,10 +144,10 @@ __device__ __forceinline__ Q8v q8_load(const float* qs, int n, int c, int li) {
 }
 
 // -------------------------------------------------------------------------
-// k_pm: left product on MFMA.  A block owns PM_ROWS whole rows; its eight
-// waves take interleaved 32-column K-steps of those rows (so together they
-// stream contiguous column ranges) and their partial tiles are summed in LDS
-// in wave order.  The block then stores its final rows of P and the fp64
+// k_pm: left product on MFMA.  A block owns PM_ROWS whole rows; its
+// PM_WAVES waves take interleaved 32-column K-steps of those rows (so
+// together they stream contiguous column ranges) and their partial tiles are
+// summed in LDS in wave order.  The block then stores its final rows of P and the fp64
 // Gram partial of those rows.
 //
 // The MFMA operand layout gives each of a load's 64 lanes a different row
@@ -136,25 +159,33 @@ __device__ __forceinline__ Q8v q8_load(const float* qs, int n, int c, int li) {
 // writes lane l's 16 bytes to LDS at base + 16 l and so lets every
 // instruction read whole 128-byte lines (8 rows of err, 16 rows of bf16 M);
 // lanes fetch their chunks in an XOR-swizzled order so that the operand
-// reads from LDS are free of bank conflicts.  Each wave owns two tile
-// stages: it waits for the K-step it is about to use, reads its operands,
-// and issues the next K-step's tile before running the products.
+// reads from LDS are free of bank conflicts.  Each wave owns PM_STAGES tile
+// stages, two K-steps in flight while it works on a third: with one block of
+// four waves per compute unit that measured faster (40.5-41 us vs 42.5 us on
+// 8192 x 4096) than eight waves with one K-step in flight each, which is
+// what the LDS allows for eight.
 // -------------------------------------------------------------------------
 constexpr int PM_ESLOT = 1024 + 128;   // LDS bytes per 8-row err load; the pad shifts banks by 32 words
 constexpr int PM_BSLOT = 1024;         // LDS bytes per 16-row bf16 M load
 constexpr int PM_QBYTES = 32 * 16 * 4; // Q rows of a K-step (rank padded to at most 16)
 constexpr int PM_STAGE = 4 * PM_ESLOT + 2 * PM_BSLOT + PM_QBYTES;   // one K-step, 32 rows x 32 columns
 
+constexpr int PM_STAGES = 3;             // K-step stages per wave (two in flight)
+
 union PMSmem {
   struct {
     float red[PM_WAVES][PM_ROWS * 16];   // per-wave partial tiles
     double rows[PM_ROWS * 16];           // final P rows as doubles (Gram)
   } e;
-  uint8_t tile[PM_WAVES][2][PM_STAGE];   // per wave, two K-step stages (bf16 M)
+  uint8_t tile[PM_WAVES][PM_STAGES][PM_STAGE];   // per wave, the K-step stages (bf16 M)
 };
 
 typedef __attribute__((address_space(1))) void gvoid_t;
 typedef __attribute__((address_space(3))) void lvoid_t;
+
+// load instructions pm_tile_issue issues per K-step (the same in every wave)
+template <int RP>
+constexpr int pm_tile_loads() { return 4 + 2 + (32 * RP * 4 + 1023) / 1024; }
 
 // K-step columns [c0, c0 + 32) of the block's 32 rows of err and bf16 M, and
 // Q rows c0 .. c0+31, into `dst` (rows past m repeat row m-1; their results
@@ -186,31 +217,6 @@ __device__ __forceinline__ void pm_tile_issue(const Desc& d, const float* qs, in
     if (1024 * q + 16 * lane < 32 * RP * 4)
       __builtin_amdgcn_global_load_lds((gvoid_t*)(qs + (int64_t)c0 * RP + 256 * q + 4 * lane),
                                        (lvoid_t*)(dst + 4 * PM_ESLOT + 2 * PM_BSLOT + 1024 * q), 16, 0, 0);
-}
-
-// Lane (g, li)'s operand chunk of row tile r (row 16 r + li, columns 8g..8g+7)
-// from a tile written by pm_tile_issue.
-__device__ __forceinline__ Ch8<DT_BF16> pm_tile_read(const uint8_t* src, int r, int li, int g) {
-  Ch8<DT_BF16> x;
-  const int q = 2 * r + (li >> 3), rr = li & 7;
-  const uint8_t* e = src + q * PM_ESLOT + rr * 128;
-  x.e0 = *(const float4*)(e + 16 * ((2 * g) ^ rr));
-  x.e1 = *(const float4*)(e + 16 * ((2 * g + 1) ^ rr));
-  x.m = *(const uint4*)(src + 4 * PM_ESLOT + r * PM_BSLOT + li * 64 + 16 * (g ^ (li >> 2)));
-  return x;
-}
-
-// Q[c0 + 8g + j][li] for j < 8 from the tile (zero past the padded rank).
-template <int RP>
-__device__ __forceinline__ Q8v pm_tile_q(const uint8_t* src, int li, int g) {
-  const float* qt = (const float*)(src + 4 * PM_ESLOT + 2 * PM_BSLOT);
-  float v[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) v[j] = li < RP ? qt[(8 * g + j) * RP + li] : 0.f;
-  Q8v q;
-  q.a = make_float4(v[0], v[1], v[2], v[3]);
-  q.b = make_float4(v[4], v[5], v[6], v[7]);
-  return q;
 }
 
 template <int DT, bool VEC, int RP>
@@ -253,22 +259,65 @@ __device__ __forceinline__ void pm_body(const Desc& d, int b, PMSmem& sm) {
   if constexpr (DT == DT_BF16 && VEC) {
     dma = d.err_in != nullptr && (d.n & 31) == 0 && ((uintptr_t)qs & 15) == 0;
     if (dma) {
-      // stage s of this wave's tiles: its own base plus s * PM_STAGE (plain
-      // offsets keep the accesses in the LDS address space)
+      // This wave's K-steps ks = wave + PM_WAVES * it; step it lives in stage
+      // it % PM_STAGES.  Per step: wait until only the steps issued after it
+      // may be in flight, read its operands (inline ds_read, see above),
+      // issue the step PM_STAGES - 1 ahead into the stage just freed, run the
+      // products.
+      constexpr int NI = pm_tile_loads<RP>();
+      static_assert(PM_STAGES <= 4 && 2 * NI <= 63, "vmcnt immediates");
       uint8_t* const tiles = sm.tile[wave][0];
-      int ks = wave;
-      if (ks < nk) pm_tile_issue<RP>(d, qs, row0, kcol(ks) - 8 * g, tiles);
-      for (int it = 0; ks < nk; ks += PM_WAVES, ++it) {
-        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        const uint8_t* cur = tiles + (it & 1) * PM_STAGE;
+      const uint32_t tbase = (uint32_t)(size_t)(lvoid_t*)tiles;
+      const int nmine = wave < nk ? (nk - wave + PM_WAVES - 1) / PM_WAVES : 0;
+#pragma unroll
+      for (int y = 0; y + 1 < PM_STAGES; ++y)
+        if (y < nmine) pm_tile_issue<RP>(d, qs, row0, kcol(wave + PM_WAVES * y) - 8 * g, tiles + y * PM_STAGE);
+      int st = 0;
+      for (int it = 0; it < nmine; ++it) {
+        const int after = min(it + PM_STAGES - 2, nmine - 1) - it;
+        if (after <= 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        else if (after == 1) asm volatile("s_waitcnt vmcnt(%0)" :: "n"(NI) : "memory");
+        else asm volatile("s_waitcnt vmcnt(%0)" :: "n"(2 * NI) : "memory");
+        const uint32_t cb = tbase + st * PM_STAGE;
+        f4v e0[PM_RB], e1[PM_RB], mm[PM_RB];
+        float qv[8];
+#pragma unroll
+        for (int r = 0; r < PM_RB; ++r) {
+          const int q = 2 * r + (li >> 3), rr = li & 7;
+          const uint32_t e = cb + q * PM_ESLOT + rr * 128;
+          ds_read_asm<4>(e0[r], e + 16 * ((2 * g) ^ rr));
+          ds_read_asm<4>(e1[r], e + 16 * ((2 * g + 1) ^ rr));
+          ds_read_asm<4>(mm[r], cb + 4 * PM_ESLOT + r * PM_BSLOT + li * 64 + 16 * (g ^ (li >> 2)));
+        }
+        const int lq = li < RP ? li : 0;
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          ds_read_asm<1>(qv[j], cb + 4 * PM_ESLOT + 2 * PM_BSLOT + ((8 * g + j) * RP + lq) * 4);
+        static_assert(PM_RB == 2, "the wait below names the operands of two row tiles");
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(e0[0]), "+v"(e1[0]), "+v"(mm[0]), "+v"(e0[1]), "+v"(e1[1]), "+v"(mm[1]),
+                       "+v"(qv[0]), "+v"(qv[1]), "+v"(qv[2]), "+v"(qv[3]), "+v"(qv[4]), "+v"(qv[5]),
+                       "+v"(qv[6]), "+v"(qv[7]));
+        if (it + PM_STAGES - 1 < nmine) {
+          const int sn = st == 0 ? PM_STAGES - 1 : st - 1;
+          pm_tile_issue<RP>(d, qs, row0, kcol(wave + PM_WAVES * (it + PM_STAGES - 1)) - 8 * g,
+                            tiles + sn * PM_STAGE);
+        }
+        st = st + 1 == PM_STAGES ? 0 : st + 1;
         Ch8<DT> x[PM_RB];
-  #pragma unroll
-        for (int r = 0; r < PM_RB; ++r) x[r] = pm_tile_read(cur, r, li, g);
-        const Q8v cq = pm_tile_q<RP>(cur, li, g);
-        const int kn = ks + PM_WAVES;
-        if (kn < nk) pm_tile_issue<RP>(d, qs, row0, kcol(kn) - 8 * g, tiles + ((it + 1) & 1) * PM_STAGE);
+#pragma unroll
+        for (int r = 0; r < PM_RB; ++r) {
+          x[r].e0 = make_float4(e0[r][0], e0[r][1], e0[r][2], e0[r][3]);
+          x[r].e1 = make_float4(e1[r][0], e1[r][1], e1[r][2], e1[r][3]);
+          x[r].m = make_uint4(__float_as_uint(mm[r][0]), __float_as_uint(mm[r][1]),
+                              __float_as_uint(mm[r][2]), __float_as_uint(mm[r][3]));
+        }
+        Q8v cq;
+        const bool qin = li < RP;
+        cq.a = make_float4(qin ? qv[0] : 0.f, qin ? qv[1] : 0.f, qin ? qv[2] : 0.f, qin ? qv[3] : 0.f);
+        cq.b = make_float4(qin ? qv[4] : 0.f, qin ? qv[5] : 0.f, qin ? qv[6] : 0.f, qin ? qv[7] : 0.f);
         mfma_step(x, cq);
-    }
+      }
     }
   }
   if (!dma) {
