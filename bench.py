@@ -72,10 +72,11 @@ def product_engine(kernel: str, m_dtype: str, rank: int) -> tuple:
 
     Ranks padded to <= 16 and fp32 inputs run fp32 products on fp32 matrix
     cores.  For bf16 M at padded ranks 32..128 the left and right products
-    run on bf16 matrix cores with split operands, three bf16 products per
-    algorithmic product, so the algorithmic flops have a third of the bf16
-    peak; the reconstruction stays on fp32 matrix cores."""
-    if m_dtype == "bf16" and rank > 16 and kernel.startswith("pass_"):
+    and the reconstruction run on bf16 matrix cores with split operands,
+    three bf16 products per algorithmic product, so the algorithmic flops
+    have a third of the bf16 peak."""
+    split = kernel.startswith(("pass_", "mhat_err", "err_only"))
+    if m_dtype == "bf16" and rank > 16 and split:
         return BF16_MFMA_PEAK_TFLOPS / 3.0, "bf16 matrix cores, split operands (3 products)"
     return FP32_MFMA_PEAK_TFLOPS, "fp32 matrix cores"
 
