@@ -165,10 +165,15 @@ __device__ __forceinline__ Q8v q8_load(const float* qs, int n, int c, int li) {
 // 8192 x 4096) than eight waves with one K-step in flight each, which is
 // what the LDS allows for eight.
 // -------------------------------------------------------------------------
-constexpr int PM_ESLOT = 1024 + 128;   // LDS bytes per 8-row err load; the pad shifts banks by 32 words
+constexpr int PM_ESLOT = 1024 + 128;   // LDS bytes per 8-row fp32 load; the pad shifts banks by 32 words
 constexpr int PM_BSLOT = 1024;         // LDS bytes per 16-row bf16 M load
 constexpr int PM_QBYTES = 32 * 16 * 4; // Q rows of a K-step (rank padded to at most 16)
-constexpr int PM_STAGE = 4 * PM_ESLOT + 2 * PM_BSLOT + PM_QBYTES;   // one K-step, 32 rows x 32 columns
+// one K-step, 32 rows x 32 columns: err, then M (bf16: two 16-row slots;
+// fp32: four 8-row slots laid out like err), then the Q rows
+template <int DT>
+constexpr int pm_mbytes() { return DT == DT_BF16 ? 2 * PM_BSLOT : 4 * PM_ESLOT; }
+template <int DT>
+constexpr int pm_stage() { return 4 * PM_ESLOT + pm_mbytes<DT>() + PM_QBYTES; }
 
 constexpr int PM_STAGES = 3;             // K-step stages per wave (two in flight)
 
@@ -177,20 +182,20 @@ union PMSmem {
     float red[PM_WAVES][PM_ROWS * 16];   // per-wave partial tiles
     double rows[PM_ROWS * 16];           // final P rows as doubles (Gram)
   } e;
-  uint8_t tile[PM_WAVES][PM_STAGES][PM_STAGE];   // per wave, the K-step stages (bf16 M)
+  uint8_t tile[PM_WAVES][PM_STAGES][pm_stage<DT_F32>()];   // per wave, the K-step stages
 };
 
 typedef __attribute__((address_space(1))) void gvoid_t;
 typedef __attribute__((address_space(3))) void lvoid_t;
 
 // load instructions pm_tile_issue issues per K-step (the same in every wave)
-template <int RP>
-constexpr int pm_tile_loads() { return 4 + 2 + (32 * RP * 4 + 1023) / 1024; }
+template <int DT, int RP>
+constexpr int pm_tile_loads() { return 4 + (DT == DT_BF16 ? 2 : 4) + (32 * RP * 4 + 1023) / 1024; }
 
-// K-step columns [c0, c0 + 32) of the block's 32 rows of err and bf16 M, and
-// Q rows c0 .. c0+31, into `dst` (rows past m repeat row m-1; their results
+// K-step columns [c0, c0 + 32) of the block's 32 rows of err and M, and Q
+// rows c0 .. c0+31, into `dst` (rows past m repeat row m-1; their results
 // are never stored).
-template <int RP>
+template <int DT, int RP>
 __device__ __forceinline__ void pm_tile_issue(const Desc& d, const float* qs, int row0, int c0,
                                               uint8_t* dst) {
   const int lane = threadIdx.x & 63;
@@ -203,20 +208,31 @@ __device__ __forceinline__ void pm_tile_issue(const Desc& d, const float* qs, in
     __builtin_amdgcn_global_load_lds((gvoid_t*)(d.err_in + (int64_t)row * d.lde_in + c0 + 4 * ch),
                                      (lvoid_t*)(dst + q * PM_ESLOT), 16, 0, 0);
   }
+  if constexpr (DT == DT_BF16) {
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    // bf16 M rows 16q .. 16q+15: lane l takes row l / 4, chunk (l % 4) ^ (l / 16)
-    const int rr = lane >> 2, ch = (lane & 3) ^ (rr >> 2);
-    const int row = min(row0 + 16 * q + rr, last);
-    __builtin_amdgcn_global_load_lds((gvoid_t*)((const uint16_t*)d.M + (int64_t)row * d.ldm + c0 + 8 * ch),
-                                     (lvoid_t*)(dst + 4 * PM_ESLOT + q * PM_BSLOT), 16, 0, 0);
+    for (int q = 0; q < 2; ++q) {
+      // bf16 M rows 16q .. 16q+15: lane l takes row l / 4, chunk (l % 4) ^ (l / 16)
+      const int rr = lane >> 2, ch = (lane & 3) ^ (rr >> 2);
+      const int row = min(row0 + 16 * q + rr, last);
+      __builtin_amdgcn_global_load_lds((gvoid_t*)((const uint16_t*)d.M + (int64_t)row * d.ldm + c0 + 8 * ch),
+                                       (lvoid_t*)(dst + 4 * PM_ESLOT + q * PM_BSLOT), 16, 0, 0);
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      // fp32 M: the err layout
+      const int rr = lane >> 3, ch = (lane & 7) ^ rr;
+      const int row = min(row0 + 8 * q + rr, last);
+      __builtin_amdgcn_global_load_lds((gvoid_t*)((const float*)d.M + (int64_t)row * d.ldm + c0 + 4 * ch),
+                                       (lvoid_t*)(dst + 4 * PM_ESLOT + q * PM_ESLOT), 16, 0, 0);
+    }
   }
   // Q rows c0 .. c0+31 (32 RP floats, contiguous) as they are
 #pragma unroll
   for (int q = 0; q < (32 * RP * 4 + 1023) / 1024; ++q)
     if (1024 * q + 16 * lane < 32 * RP * 4)
       __builtin_amdgcn_global_load_lds((gvoid_t*)(qs + (int64_t)c0 * RP + 256 * q + 4 * lane),
-                                       (lvoid_t*)(dst + 4 * PM_ESLOT + 2 * PM_BSLOT + 1024 * q), 16, 0, 0);
+                                       (lvoid_t*)(dst + 4 * PM_ESLOT + pm_mbytes<DT>() + 1024 * q), 16, 0, 0);
 }
 
 template <int DT, bool VEC, int RP>
@@ -252,11 +268,11 @@ __device__ __forceinline__ void pm_body(const Desc& d, int b, PMSmem& sm) {
     }
   };
 
-  // bf16 M with 16-byte aligned rows, whole 32-column K-steps and a 16-byte
-  // aligned Q: tiles through LDS (the condition is the same for the whole
-  // launch); otherwise loads straight into registers.
+  // 16-byte aligned rows, whole 32-column K-steps, an error buffer and a
+  // 16-byte aligned Q: tiles through LDS (the condition is the same for the
+  // whole launch); otherwise loads straight into registers.
   bool dma = false;
-  if constexpr (DT == DT_BF16 && VEC) {
+  if constexpr (VEC) {
     dma = d.err_in != nullptr && (d.n & 31) == 0 && ((uintptr_t)qs & 15) == 0;
     if (dma) {
       // This wave's K-steps ks = wave + PM_WAVES * it; step it lives in stage
@@ -264,22 +280,25 @@ __device__ __forceinline__ void pm_body(const Desc& d, int b, PMSmem& sm) {
       // may be in flight, read its operands (inline ds_read, see above),
       // issue the step PM_STAGES - 1 ahead into the stage just freed, run the
       // products.
-      constexpr int NI = pm_tile_loads<RP>();
+      constexpr int NI = pm_tile_loads<DT, RP>();
+      constexpr int STAGE = pm_stage<DT>();
       static_assert(PM_STAGES <= 4 && 2 * NI <= 63, "vmcnt immediates");
       uint8_t* const tiles = sm.tile[wave][0];
       const uint32_t tbase = (uint32_t)(size_t)(lvoid_t*)tiles;
       const int nmine = wave < nk ? (nk - wave + PM_WAVES - 1) / PM_WAVES : 0;
 #pragma unroll
       for (int y = 0; y + 1 < PM_STAGES; ++y)
-        if (y < nmine) pm_tile_issue<RP>(d, qs, row0, kcol(wave + PM_WAVES * y) - 8 * g, tiles + y * PM_STAGE);
+        if (y < nmine) pm_tile_issue<DT, RP>(d, qs, row0, kcol(wave + PM_WAVES * y) - 8 * g, tiles + y * STAGE);
       int st = 0;
       for (int it = 0; it < nmine; ++it) {
         const int after = min(it + PM_STAGES - 2, nmine - 1) - it;
         if (after <= 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         else if (after == 1) asm volatile("s_waitcnt vmcnt(%0)" :: "n"(NI) : "memory");
         else asm volatile("s_waitcnt vmcnt(%0)" :: "n"(2 * NI) : "memory");
-        const uint32_t cb = tbase + st * PM_STAGE;
-        f4v e0[PM_RB], e1[PM_RB], mm[PM_RB];
+        const uint32_t cb = tbase + st * STAGE;
+        // err (and fp32 M) of row tile r: row 16 r + li is slot 2r + li/8,
+        // row li % 8 of it; chunk c of that row sits at c ^ (li % 8)
+        f4v e0[PM_RB], e1[PM_RB], m0[PM_RB], m1[PM_RB];
         float qv[8];
 #pragma unroll
         for (int r = 0; r < PM_RB; ++r) {
@@ -287,21 +306,33 @@ __device__ __forceinline__ void pm_body(const Desc& d, int b, PMSmem& sm) {
           const uint32_t e = cb + q * PM_ESLOT + rr * 128;
           ds_read_asm<4>(e0[r], e + 16 * ((2 * g) ^ rr));
           ds_read_asm<4>(e1[r], e + 16 * ((2 * g + 1) ^ rr));
-          ds_read_asm<4>(mm[r], cb + 4 * PM_ESLOT + r * PM_BSLOT + li * 64 + 16 * (g ^ (li >> 2)));
+          if constexpr (DT == DT_BF16) {
+            ds_read_asm<4>(m0[r], cb + 4 * PM_ESLOT + r * PM_BSLOT + li * 64 + 16 * (g ^ (li >> 2)));
+          } else {
+            ds_read_asm<4>(m0[r], e + 4 * PM_ESLOT + 16 * ((2 * g) ^ rr));
+            ds_read_asm<4>(m1[r], e + 4 * PM_ESLOT + 16 * ((2 * g + 1) ^ rr));
+          }
         }
         const int lq = li < RP ? li : 0;
 #pragma unroll
         for (int j = 0; j < 8; ++j)
-          ds_read_asm<1>(qv[j], cb + 4 * PM_ESLOT + 2 * PM_BSLOT + ((8 * g + j) * RP + lq) * 4);
-        static_assert(PM_RB == 2, "the wait below names the operands of two row tiles");
-        asm volatile("s_waitcnt lgkmcnt(0)"
-                     : "+v"(e0[0]), "+v"(e1[0]), "+v"(mm[0]), "+v"(e0[1]), "+v"(e1[1]), "+v"(mm[1]),
-                       "+v"(qv[0]), "+v"(qv[1]), "+v"(qv[2]), "+v"(qv[3]), "+v"(qv[4]), "+v"(qv[5]),
-                       "+v"(qv[6]), "+v"(qv[7]));
+          ds_read_asm<1>(qv[j], cb + 4 * PM_ESLOT + pm_mbytes<DT>() + ((8 * g + j) * RP + lq) * 4);
+        static_assert(PM_RB == 2, "the waits below name the operands of two row tiles");
+        if constexpr (DT == DT_BF16) {
+          asm volatile("s_waitcnt lgkmcnt(0)"
+                       : "+v"(e0[0]), "+v"(e1[0]), "+v"(m0[0]), "+v"(e0[1]), "+v"(e1[1]), "+v"(m0[1]),
+                         "+v"(qv[0]), "+v"(qv[1]), "+v"(qv[2]), "+v"(qv[3]), "+v"(qv[4]), "+v"(qv[5]),
+                         "+v"(qv[6]), "+v"(qv[7]));
+        } else {
+          asm volatile("s_waitcnt lgkmcnt(0)"
+                       : "+v"(e0[0]), "+v"(e1[0]), "+v"(m0[0]), "+v"(m1[0]), "+v"(e0[1]), "+v"(e1[1]),
+                         "+v"(m0[1]), "+v"(m1[1]), "+v"(qv[0]), "+v"(qv[1]), "+v"(qv[2]), "+v"(qv[3]),
+                         "+v"(qv[4]), "+v"(qv[5]), "+v"(qv[6]), "+v"(qv[7]));
+        }
         if (it + PM_STAGES - 1 < nmine) {
           const int sn = st == 0 ? PM_STAGES - 1 : st - 1;
-          pm_tile_issue<RP>(d, qs, row0, kcol(wave + PM_WAVES * (it + PM_STAGES - 1)) - 8 * g,
-                            tiles + sn * PM_STAGE);
+          pm_tile_issue<DT, RP>(d, qs, row0, kcol(wave + PM_WAVES * (it + PM_STAGES - 1)) - 8 * g,
+                                tiles + sn * STAGE);
         }
         st = st + 1 == PM_STAGES ? 0 : st + 1;
         Ch8<DT> x[PM_RB];
@@ -309,8 +340,13 @@ __device__ __forceinline__ void pm_body(const Desc& d, int b, PMSmem& sm) {
         for (int r = 0; r < PM_RB; ++r) {
           x[r].e0 = make_float4(e0[r][0], e0[r][1], e0[r][2], e0[r][3]);
           x[r].e1 = make_float4(e1[r][0], e1[r][1], e1[r][2], e1[r][3]);
-          x[r].m = make_uint4(__float_as_uint(mm[r][0]), __float_as_uint(mm[r][1]),
-                              __float_as_uint(mm[r][2]), __float_as_uint(mm[r][3]));
+          if constexpr (DT == DT_BF16) {
+            x[r].m = make_uint4(__float_as_uint(m0[r][0]), __float_as_uint(m0[r][1]),
+                                __float_as_uint(m0[r][2]), __float_as_uint(m0[r][3]));
+          } else {
+            x[r].m0 = make_float4(m0[r][0], m0[r][1], m0[r][2], m0[r][3]);
+            x[r].m1 = make_float4(m1[r][0], m1[r][1], m1[r][2], m1[r][3]);
+          }
         }
         Q8v cq;
         const bool qin = li < RP;

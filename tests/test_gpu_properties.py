@@ -91,16 +91,17 @@ def test_split_decompress_close_to_fp32(rank):
     assert rel_b <= 1e-4
 
 
-@pytest.mark.parametrize("rank,n", [(8, 200), (64, 200), (8, 224), (16, 512)])
-def test_compress_without_error_buffer(rank, n):
-    """No error buffer equals a zero one bit for bit.  At rank <= 16 with bf16
-    M and whole 32-column K-steps (n = 224, 512) the zero buffer takes the
-    left product's LDS-tile path and no buffer the register path, so this
-    also pins the tile layout to the register loads."""
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("rank,n", [(8, 200), (64, 200), (8, 224), (16, 512), (4, 96)])
+def test_compress_without_error_buffer(rank, n, dtype):
+    """No error buffer equals a zero one bit for bit.  At rank <= 16 with
+    whole 32-column K-steps (n = 96, 224, 512) the zero buffer takes the left
+    product's LDS-tile path and no buffer the register path, so this also
+    pins the tile layouts (bf16 and fp32 M) to the register loads."""
     from paper_2301_09830_amd import optcc
     torch = torch_mod()
-    w, M, q0 = _inputs(m=300, n=n, rank=rank)
-    Md = to_device(M, "bf16")
+    w, M, q0 = _inputs(m=300, n=n, rank=rank, dtype=dtype)
+    Md = to_device(M, dtype)
     Qa = torch.from_numpy(q0).cuda()
     Qb = Qa.clone()
     zero = torch.zeros(M.shape, device="cuda")
