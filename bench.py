@@ -8,7 +8,12 @@ occ_step call: error-feedback add, left product, CholeskyQR, right product,
 reconstruction and residual.
 
 Prints ONE JSON line.  `value` is input GB/s (bytes of M as stored, per step,
-over the measured step time) with every input already resident in HBM.
+over the measured step time) with every input already resident in HBM, from
+K back-to-back steps between two synchronisations.  `cold` repeats the step
+at least 20 times, each with its own event pair after a read of an unrelated
+2 GiB buffer outside the events (the caches then hold clean, unrelated data),
+and reports the median; `step_roofline` and `cold.step_roofline_frac` are the
+two step-level fractions of the 8 TB/s HBM roofline.
 `roofline` is measured for the kernel that takes the most time, from HIP
 events bracketing each of its launches on the library's stream, against the
 8 TB/s HBM3E peak; `traffic` comes from the committed rocprofv3 counter
@@ -145,38 +150,69 @@ def to_device(x, dtype: str):
     return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).cuda()
 
 
-def cpu_baseline(w, host, seconds: float):
-    """Time oracle.step on this host's cores over a bounded sample."""
-    import numpy as np
+def host_info() -> dict:
+    """CPU model of this host and the BLAS library numpy runs on."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    blas, threads = "unknown", 1
     try:
         from threadpoolctl import threadpool_info
-        cores = max((i.get("num_threads", 1) for i in threadpool_info()), default=1)
-    except Exception:
-        cores = int(os.environ.get("OMP_NUM_THREADS", "1"))
-    import oracle
-    count = len(w.shapes)
-    state = {j: (np.zeros(w.shapes[j]), w.q0(j).astype(np.float64)) for j in range(count)}
-    n_inputs = len({s for (s, _) in host})
-    done_bytes, steps, mats = 0, 0, 0
-    t0 = time.perf_counter()
-    while True:
-        s = steps % n_inputs
-        for j in range(count):
-            e, q = state[j]
-            out = oracle.step(host[(s, j)], w.m_dtype, e, q, w.rank, w.iters)
-            state[j] = (out["err"], out["Q"])
-            done_bytes += host[(s, j)].nbytes
-            mats += 1
-            if time.perf_counter() - t0 > seconds:
+        for i in threadpool_info():
+            if i.get("user_api") == "blas":
+                blas = f"{i.get('internal_api')} {i.get('version')} ({i.get('architecture')})"
+                threads = int(i.get("num_threads", 1))
                 break
-        steps += 1
-        if time.perf_counter() - t0 > seconds:
-            break
-    dt = time.perf_counter() - t0
-    return {"value": round(done_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": int(cores),
-            "kind": "oracle", "seconds": round(dt, 2),
-            "sample": f"{mats} matrix steps of {w.name} (oracle.step, float64, "
-                      f"carried err/Q) on {cores} BLAS threads"}
+    except Exception:
+        threads = int(os.environ.get("OMP_NUM_THREADS", "1"))
+    return {"cpu_model": model, "blas": blas, "cores": threads}
+
+
+def cpu_baseline(w, host, seconds: float, runs: int = 3):
+    """Time oracle.step on this host's cores: `runs` runs of about
+    seconds / runs each over the same bounded sample (whole matrix steps,
+    err and Q carried from the workload's initial state), reporting the
+    median input GB/s."""
+    import numpy as np
+    import oracle
+    info = host_info()
+    count = len(w.shapes)
+    n_inputs = len({s for (s, _) in host})
+    rates, mats_done, spent = [], [], 0.0
+    for _ in range(runs):
+        state = {j: (np.zeros(w.shapes[j]), w.q0(j).astype(np.float64)) for j in range(count)}
+        done_bytes, steps, mats = 0, 0, 0
+        t0 = time.perf_counter()
+        while True:
+            s = steps % n_inputs
+            for j in range(count):
+                e, q = state[j]
+                out = oracle.step(host[(s, j)], w.m_dtype, e, q, w.rank, w.iters)
+                state[j] = (out["err"], out["Q"])
+                done_bytes += host[(s, j)].nbytes
+                mats += 1
+                if time.perf_counter() - t0 > seconds / runs:
+                    break
+            steps += 1
+            if time.perf_counter() - t0 > seconds / runs:
+                break
+        dt = time.perf_counter() - t0
+        spent += dt
+        rates.append(done_bytes / dt / 1e9)
+        mats_done.append(mats)
+    med = sorted(rates)[len(rates) // 2]
+    return {"value": round(med, 4), "unit": "GB/s", "cores": info["cores"],
+            "kind": "oracle", "seconds": round(spent, 2),
+            "runs_gbs": [round(r, 4) for r in rates],
+            "cpu_model": info["cpu_model"], "blas": info["blas"],
+            "sample": f"median of {runs} runs of {'/'.join(str(x) for x in mats_done)} matrix "
+                      f"steps of {w.name} (oracle.step, float64, err/Q carried from the initial "
+                      f"state) on {info['cores']} BLAS threads"}
 
 
 # ----------------------------------------------------------------------------
@@ -323,7 +359,11 @@ def main() -> int:
     ap.add_argument("--inputs", type=int, default=0,
                     help="distinct seeded inputs cycled through (default: the workload's steps)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cold-reps", type=int, default=30,
+                    help="flushed repetitions (median reported; at least 20)")
+    ap.add_argument("--flush-gib", type=float, default=2.0,
+                    help="bytes read between flushed repetitions, GiB (at least 1)")
     ap.add_argument("--no-kernel-timing", action="store_true")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="also run a plain device copy of this size (counter calibration)")
@@ -406,6 +446,35 @@ def main() -> int:
     value = input_bytes / (ms_per_step * 1e-3) / 1e9
     step_bytes = step_alg_bytes(elements, m_bytes, w.iters)
 
+    # Flushed ("cold") steps: before each repetition, outside its events, read
+    # a buffer of flush_gib GiB (larger than the 256 MiB memory-side cache and
+    # the 8 x 4 MiB L2), so every repetition starts with caches holding clean,
+    # unrelated data; median over the repetitions.
+    cold = None
+    if args.cold_reps > 0:
+        reps = max(20, args.cold_reps)
+        flush = torch.empty(int(max(1.0, args.flush_gib) * (1 << 30)) // 4, dtype=torch.float32,
+                            device="cuda").fill_(1.0)
+        sink = torch.zeros((), dtype=torch.float32, device="cuda")
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(reps)]
+        torch.cuda.synchronize()
+        for k in range(reps):
+            sink += flush.sum()
+            evs[k][0].record(stream)
+            step(args.warmup + args.steps + k)
+            evs[k][1].record(stream)
+        torch.cuda.synchronize()
+        times = sorted(a.elapsed_time(b) for a, b in evs)
+        med = times[len(times) // 2]
+        cold = {"ms_per_step_median": round(med, 5), "ms_min": round(times[0], 5),
+                "ms_max": round(times[-1], 5), "reps": reps,
+                "value": round(input_bytes / (med * 1e-3) / 1e9, 2),
+                "step_roofline_frac": round(step_bytes / (med * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                "flush": f"{flush.numel() * 4 / (1 << 30):.1f} GiB read (torch sum) before each "
+                         "repetition, outside its events"}
+        del flush
+
     kernels = {}
     roofline = None
     if not args.no_kernel_timing:
@@ -438,9 +507,18 @@ def main() -> int:
                 achieved, peak, unit = flops / avg_s / 1e12, round(mfma_peak, 1), "TFLOP/s"
             else:
                 achieved, peak, unit = per_launch / avg_s / 1e9, HBM_PEAK_GBS, "GB/s"
+            # the committed kernel trace of the same kernel and workload, side by side
+            trace_us = None if prof_rec is None else prof_rec.get("avg_duration_us")
+            trace_frac = None
+            if trace_us:
+                t_s = trace_us * 1e-6
+                trace_frac = round((flops / t_s / 1e12 if mfma_bound else per_launch / t_s / 1e9)
+                                   / (mfma_peak if mfma_bound else HBM_PEAK_GBS), 4)
             roofline = {"kernel": dom, "bound": "mfma" if mfma_bound else "hbm",
                         "achieved": round(achieved, 1), "peak": peak, "unit": unit,
                         "frac": round(achieved / peak, 4),
+                        "frac_source": "HIP events bracketing each launch in this run",
+                        "trace_avg_us": trace_us, "trace_frac": trace_frac,
                         "traffic": traffic, "alg_bytes_per_launch": int(per_launch),
                         "alg_flops_per_launch": flops, "engine": engine,
                         "mfma_util": (prof_rec or {}).get("mfma", {}).get("util"),
@@ -477,7 +555,9 @@ def main() -> int:
                    "distinct_inputs": n_inputs, "state": "err and Q carried across steps"},
         "step_roofline": {"alg_bytes_per_step": step_bytes,
                           "achieved": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
-                          "frac": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+                          "frac": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                          "timing": "back-to-back steps (warm caches)"},
+        "cold": cold,
         "roofline": roofline,
         "cpu_baseline": cpu,
         "kernels": kernels,

@@ -53,7 +53,7 @@
 extern "C" {
 #endif
 
-#define OCC_ABI_VERSION 1
+#define OCC_ABI_VERSION 2
 #define OCC_MAX_RANK 128
 #define OCC_MAX_ITERS 64
 
@@ -80,6 +80,17 @@ enum { OCC_F_NONFINITE = 1u, OCC_F_RANK_DEFICIENT = 2u };
 
 /* call flags for occ_step / occ_step_batched */
 enum { OCC_NO_MHAT = 1u }; /* sender side: do not write M_hat (err is still updated) */
+
+/* flags of occ_decompress_ex */
+enum {
+  /* run the products occ_step runs for a bf16 M: at padded ranks 32..128 on
+   * bf16 matrix cores with each factor split into two bf16 parts (about 2^-16
+   * of |M_hat| per element); at padded rank <= 16 the products are fp32 either
+   * way and the flag changes nothing */
+  OCC_DEC_SPLIT_BF16 = 1u,
+  /* store M_hat as bf16 (round to nearest even from the fp32 result) */
+  OCC_DEC_OUT_BF16 = 2u
+};
 
 /* One matrix and its compressor state.
  *   M      input gradient, rows x cols, leading dimension ldm, dtype m_dtype
@@ -113,8 +124,10 @@ const char* occ_status_str(int status);
  * depend on the pointers.  Returns 0 for invalid arguments. */
 size_t occ_workspace_bytes(const occ_mat_t* mats, int count, int rank, int iters);
 
-/* Workspace bytes occ_compress needs for one m x n matrix. */
-size_t occ_compress_workspace_bytes(int64_t m, int64_t n, int rank, int iters);
+/* Workspace bytes occ_compress needs for one m x n matrix whose M has dtype
+ * m_dtype (the tiling of the large-rank passes depends on it).  Returns 0 for
+ * invalid arguments. */
+size_t occ_compress_workspace_bytes(int64_t m, int64_t n, int m_dtype, int rank, int iters);
 
 /* Clear the workspace header (sticky flags) on `stream`.  Call once after
  * allocating a workspace; the rest of the workspace needs no initialisation. */
@@ -129,24 +142,36 @@ occ_status_t occ_compress(const void* M, int m_dtype, int64_t m, int64_t n, int6
                           int rank, int iters, void* ws, size_t ws_bytes,
                           occ_stream_t stream);
 
-/* Decompression (Sec. 9.6): M_hat = P Q^T with P m x rank and Q n x rank.
- * m_dtype names the dtype of the M the factors were computed from and selects
- * the same products occ_step uses for it: for OCC_BF16 at ranks above 16 the
- * factors are split into two bf16 parts each (about 2^-16 of |M_hat| per
- * element, inside bf16 input precision), otherwise fp32 products. */
+/* Decompression (Sec. 9.6): M_hat = P Q^T with P m x rank and Q n x rank,
+ * fp32 products with fp32 accumulation, M_hat fp32 (m x n, ld ldh). */
 occ_status_t occ_decompress(const float* P, const float* Q, int64_t m, int64_t n, int rank,
-                            int m_dtype, float* M_hat, int64_t ldh, occ_stream_t stream);
+                            float* M_hat, int64_t ldh, occ_stream_t stream);
+
+/* Decompression on the receiving side of compressed backpropagation (Sec. 5:
+ * the next pipeline stage rebuilds the activation gradient from the two
+ * factors it received and continues its backward pass with it).  As
+ * occ_decompress, with `flags` (OCC_DEC_*):
+ *   OCC_DEC_SPLIT_BF16  the products occ_step runs for a bf16 M, so that
+ *                       M_hat is bitwise the one the fused step writes;
+ *   OCC_DEC_OUT_BF16    M_hat is stored as bf16 (M_hat points to uint16 bf16
+ *                       bit patterns, ld ldh elements): each element is the
+ *                       fp32 result rounded to nearest even, relative error
+ *                       at most 2^-9 per element.
+ * Unknown flag bits return OCC_E_FLAGS. */
+occ_status_t occ_decompress_ex(const float* P, const float* Q, int64_t m, int64_t n, int rank,
+                               unsigned flags, void* M_hat, int64_t ldh, occ_stream_t stream);
 
 /* Error update (Sec. 5.1): err_new = (M + err_prev) - M_hat, elementwise.
- * err_new may equal err_prev (in place, same ld); err_prev NULL means zero. */
+ * err_prev and err_new share the leading dimension lde; err_new may equal
+ * err_prev (in place); err_prev NULL means zero (lde is then err_new's). */
 occ_status_t occ_err_update(const void* M, int m_dtype, int64_t m, int64_t n, int64_t ldm,
                             const float* err_prev, int64_t lde, const float* M_hat,
-                            int64_t ldh, float* err_new, int64_t lde_new,
-                            occ_stream_t stream);
+                            int64_t ldh, float* err_new, occ_stream_t stream);
 
 /* Fused compress + decompress + error update of one matrix; err is updated
- * in place.  Bitwise equal to occ_compress, occ_decompress, occ_err_update
- * called in sequence on the same inputs. */
+ * in place.  Bitwise equal to occ_compress, occ_decompress_ex (with
+ * OCC_DEC_SPLIT_BF16 when M is bf16) and occ_err_update called in sequence on
+ * the same inputs. */
 occ_status_t occ_step(const occ_mat_t* mat, int rank, int iters, unsigned flags,
                       void* ws, size_t ws_bytes, occ_stream_t stream);
 

@@ -493,6 +493,61 @@ occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, h
 
 }  // namespace
 
+namespace {
+
+// Stand-alone decompression: M_hat = P Q^T with the reconstruction kernels of
+// the fused step (SRC 1: factors from the caller's P and Q).
+template <bool OUTBF>
+occ_status_t decompress_impl(const float* P, const float* Q, int64_t m, int64_t n, int rank,
+                             bool split, void* M_hat, int64_t ldh, hipStream_t s) {
+  OCC_TRY(check_shape(m, n, ldh));
+  if (rank < 1 || rank > OCC_MAX_RANK || rank > m || rank > n) return OCC_E_RANK;
+  if (!P || !Q || !M_hat) return OCC_E_NULL;
+  const size_t es = OUTBF ? 2 : 4;
+  if (!aligned(P, 4) || !aligned(Q, 4) || !aligned(M_hat, es)) return OCC_E_ALIGN;
+  std::vector<Span> spans = {span2d(P, m, rank, rank, 4, false), span2d(Q, n, rank, rank, 4, false),
+                             span2d(M_hat, m, n, ldh, es, true)};
+  if (overlaps(spans)) return OCC_E_ALIAS;
+  const int rp = padded_rank(rank);
+  const Tiling t = make_tiling(m, n, rp);
+  Desc d{};
+  d.m = (int32_t)m;
+  d.n = (int32_t)n;
+  d.r = rank;
+  d.P = const_cast<float*>(P);
+  d.Q = const_cast<float*>(Q);
+  d.Mhat = (float*)M_hat;
+  d.ldh = (int32_t)ldh;
+  d.mr = t.mr;
+  // 4 consecutive elements per vector store: 16 bytes (fp32) or 8 (bf16)
+  const bool vec = aligned(M_hat, 4 * es) && ldh % 4 == 0;
+  occ_status_t st = OCC_OK;
+  with_rp(rp, [&](auto RPc) {
+    constexpr int RP = decltype(RPc)::value;
+    st = launch(OUTBF ? "decompress_bf16" : "decompress", s, [&] {
+      const dim3 grid(grid_of(t.blocks[K_MHAT]));
+      if constexpr (RP > kFusedMaxRank) {
+        if (split)
+          hipLaunchKernelGGL((k_mlx<RP, 1, true, false, OUTBF>), grid, dim3(kBlock), 0, s,
+                             (const Desc*)nullptr, 1, d);
+        else
+          hipLaunchKernelGGL((k_ml<DT_F32, RP, SA_SAVED, 1, true, false, OUTBF>), grid,
+                             dim3(kBlock), 0, s, (const Desc*)nullptr, 1, d);
+      } else if (vec) {
+        // same code as the fused step's reconstruction pass
+        hipLaunchKernelGGL((k_mh16<DT_F32, true, RP, 1, true, false, OUTBF>), grid, dim3(kBlock),
+                           0, s, (const Desc*)nullptr, 1, d);
+      } else {
+        hipLaunchKernelGGL((k_mh16<DT_F32, false, RP, 1, true, false, OUTBF>), grid,
+                           dim3(kBlock), 0, s, (const Desc*)nullptr, 1, d);
+      }
+    });
+  });
+  return st;
+}
+
+}  // namespace
+
 // ============================================================================
 // C ABI
 // ============================================================================
@@ -523,12 +578,12 @@ size_t occ_workspace_bytes(const occ_mat_t* mats, int count, int rank, int iters
   return b.ws_needed;
 }
 
-size_t occ_compress_workspace_bytes(int64_t m, int64_t n, int rank, int iters) {
+size_t occ_compress_workspace_bytes(int64_t m, int64_t n, int m_dtype, int rank, int iters) {
   occ_mat_t a{};
   a.rows = m;
   a.cols = n;
   a.ldm = n;
-  a.m_dtype = OCC_F32;
+  a.m_dtype = m_dtype;
   return occ_workspace_bytes(&a, 1, rank, iters);
 }
 
@@ -602,73 +657,35 @@ occ_status_t occ_compress(const void* M, int m_dtype, int64_t m, int64_t n, int6
 }
 
 occ_status_t occ_decompress(const float* P, const float* Q, int64_t m, int64_t n, int rank,
-                            int m_dtype, float* M_hat, int64_t ldh, occ_stream_t stream) {
-  if (m_dtype != OCC_F32 && m_dtype != OCC_BF16) return OCC_E_DTYPE;
-  OCC_TRY(check_shape(m, n, ldh));
-  if (rank < 1 || rank > OCC_MAX_RANK || rank > m || rank > n) return OCC_E_RANK;
-  if (!P || !Q || !M_hat) return OCC_E_NULL;
-  if (!aligned(P, 4) || !aligned(Q, 4) || !aligned(M_hat, 4)) return OCC_E_ALIGN;
-  std::vector<Span> spans = {span2d(P, m, rank, rank, 4, false), span2d(Q, n, rank, rank, 4, false),
-                             span2d(M_hat, m, n, ldh, 4, true)};
-  if (overlaps(spans)) return OCC_E_ALIAS;
-  const int rp = padded_rank(rank);
-  const Tiling t = make_tiling(m, n, rp);
-  Desc d{};
-  d.m = (int32_t)m;
-  d.n = (int32_t)n;
-  d.r = rank;
-  d.P = const_cast<float*>(P);
-  d.Q = const_cast<float*>(Q);
-  d.Mhat = M_hat;
-  d.ldh = (int32_t)ldh;
-  d.mr = t.mr;
-  const bool vec = aligned(M_hat, 16) && ldh % 4 == 0;
-  hipStream_t s = (hipStream_t)stream;
-  occ_status_t st = OCC_OK;
-  with_rp(rp, [&](auto RPc) {
-    constexpr int RP = decltype(RPc)::value;
-    st = launch("decompress", s, [&] {
-      if constexpr (RP > kFusedMaxRank) {
-        // same products as the fused step's reconstruction pass for this M dtype
-        if (m_dtype == OCC_BF16)
-          hipLaunchKernelGGL((k_mlx<RP, 1, true, false>), dim3(grid_of(t.blocks[K_MHAT])),
-                             dim3(kBlock), 0, s, (const Desc*)nullptr, 1, d);
-        else
-          hipLaunchKernelGGL((k_ml<DT_F32, RP, SA_SAVED, 1, true, false>),
-                             dim3(grid_of(t.blocks[K_MHAT])), dim3(kBlock), 0, s,
-                             (const Desc*)nullptr, 1, d);
-      } else if (vec) {
-        // same code as the fused step's reconstruction pass
-        hipLaunchKernelGGL((k_mh16<DT_F32, true, RP, 1, true, false>),
-                           dim3(grid_of(t.blocks[K_MHAT])), dim3(kBlock), 0, s,
-                           (const Desc*)nullptr, 1, d);
-      } else {
-        hipLaunchKernelGGL((k_mh16<DT_F32, false, RP, 1, true, false>),
-                           dim3(grid_of(t.blocks[K_MHAT])), dim3(kBlock), 0, s,
-                           (const Desc*)nullptr, 1, d);
-      }
-    });
-  });
-  return st;
+                            float* M_hat, int64_t ldh, occ_stream_t stream) {
+  return decompress_impl<false>(P, Q, m, n, rank, false, M_hat, ldh, (hipStream_t)stream);
+}
+
+occ_status_t occ_decompress_ex(const float* P, const float* Q, int64_t m, int64_t n, int rank,
+                               unsigned flags, void* M_hat, int64_t ldh, occ_stream_t stream) {
+  if (flags & ~(unsigned)(OCC_DEC_SPLIT_BF16 | OCC_DEC_OUT_BF16)) return OCC_E_FLAGS;
+  const bool split = (flags & OCC_DEC_SPLIT_BF16) != 0;
+  if (flags & OCC_DEC_OUT_BF16)
+    return decompress_impl<true>(P, Q, m, n, rank, split, M_hat, ldh, (hipStream_t)stream);
+  return decompress_impl<false>(P, Q, m, n, rank, split, M_hat, ldh, (hipStream_t)stream);
 }
 
 occ_status_t occ_err_update(const void* M, int m_dtype, int64_t m, int64_t n, int64_t ldm,
                             const float* err_prev, int64_t lde, const float* M_hat, int64_t ldh,
-                            float* err_new, int64_t lde_new, occ_stream_t stream) {
+                            float* err_new, occ_stream_t stream) {
   if (m_dtype != OCC_F32 && m_dtype != OCC_BF16) return OCC_E_DTYPE;
   OCC_TRY(check_shape(m, n, ldm));
   OCC_TRY(check_shape(m, n, ldh));
-  OCC_TRY(check_shape(m, n, lde_new));
-  if (err_prev) OCC_TRY(check_shape(m, n, lde));
+  OCC_TRY(check_shape(m, n, lde));
   if (!M || !M_hat || !err_new) return OCC_E_NULL;
   const size_t es = elem_size(m_dtype);
   if (!aligned(M, es) || !aligned(M_hat, 4) || !aligned(err_new, 4) ||
       (err_prev && !aligned(err_prev, 4)))
     return OCC_E_ALIGN;
+  const int64_t lde_new = lde;
   std::vector<Span> spans = {span2d(M, m, n, ldm, es, false), span2d(M_hat, m, n, ldh, 4, false),
                              span2d(err_new, m, n, lde_new, 4, true)};
   const bool inplace = err_prev && (const void*)err_prev == (const void*)err_new;
-  if (inplace && lde != lde_new) return OCC_E_ALIAS;
   if (err_prev && !inplace) spans.push_back(span2d(err_prev, m, n, lde, 4, false));
   if (overlaps(spans)) return OCC_E_ALIAS;
   Desc d{};

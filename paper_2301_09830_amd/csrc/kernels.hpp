@@ -33,6 +33,22 @@ __device__ __forceinline__ int wave_id() {
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
+// bf16 bit pattern of an fp32 value, rounded to nearest even (NaN stays NaN).
+__device__ __forceinline__ uint16_t bf16_rne(float v) {
+  return __builtin_bit_cast(uint16_t, (__bf16)v);
+}
+
+__device__ __forceinline__ uint32_t bf16_pack2(float lo, float hi) {
+  return (uint32_t)bf16_rne(lo) | ((uint32_t)bf16_rne(hi) << 16);
+}
+
+// One element of M_hat at offset `off` (elements): fp32, or bf16 when OUTBF.
+template <bool OUTBF, class D>
+__device__ __forceinline__ void store_mhat1(const D& d, int64_t off, float v) {
+  if constexpr (OUTBF) ((uint16_t*)d.Mhat)[off] = bf16_rne(v);
+  else d.Mhat[off] = v;
+}
+
 // Element (row, col) of M as fp32 (exact widening for bf16).
 template <int DT>
 __device__ __forceinline__ float m_elem(const Desc& d, int64_t off) {

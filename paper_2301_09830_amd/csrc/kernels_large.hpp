@@ -1619,6 +1619,14 @@ __global__ __launch_bounds__(kBlock) void k_lqx(OCC_KARGS) {
 #undef B_
 }
 
+// One element of M_hat, nontemporal: fp32, or bf16 (round to nearest even)
+// when OUTBF (stand-alone decompression only).
+template <bool OUTBF>
+__device__ __forceinline__ void store_mhat_nt(const Desc& d, int64_t off, float v) {
+  if constexpr (OUTBF) __builtin_nontemporal_store(bf16_rne(v), (uint16_t*)d.Mhat + off);
+  else __builtin_nontemporal_store(v, d.Mhat + off);
+}
+
 // -------------------------------------------------------------------------
 // k_ml: M_hat = P_hat Q^T, err = A - M_hat for one column tile and d.mr rows.
 // SRC 0: P_hat from phat_t, Q from qpad (fused step).  SRC 1: the caller's P
@@ -1639,7 +1647,7 @@ __device__ __forceinline__ void lm_stage_direct(const Desc& d, int row0, float (
   }
 }
 
-template <int DT, int RP, int SA, int SRC, bool WM, bool WE>
+template <int DT, int RP, int SA, int SRC, bool WM, bool WE, bool OUTBF = false>
 __device__ __forceinline__ void lm_body(const Desc& d, int b, LMSmem<RP>& sm) {
   constexpr int NCT = lm_tiles(RP), KP = RP / 2, BC = lm_block_cols(RP);
   constexpr int SF = RP * 8 / kBlock;   // float4s per thread per P_hat tile
@@ -1719,7 +1727,7 @@ __device__ __forceinline__ void lm_body(const Desc& d, int b, LMSmem<RP>& sm) {
         const int row = row0 + mf32_row(v, g);
         if (row < r_hi && col < d.n) {
           const float mh = acc[c][v];
-          if (WM) __builtin_nontemporal_store(mh, d.Mhat + (int64_t)row * d.ldh + col);
+          if (WM) store_mhat_nt<OUTBF>(d, (int64_t)row * d.ldh + col, mh);
           if (WE) {
             const float e = rawa_val<DT, SA, 1>(av[c][v], 0) - mh;
             __builtin_nontemporal_store(e, d.err_out + (int64_t)row * d.lde_out + col);
@@ -1742,10 +1750,10 @@ __device__ __forceinline__ void lm_body(const Desc& d, int b, LMSmem<RP>& sm) {
   }
 }
 
-template <int DT, int RP, int SA, int SRC, bool WM, bool WE>
+template <int DT, int RP, int SA, int SRC, bool WM, bool WE, bool OUTBF = false>
 __global__ __launch_bounds__(kBlock) void k_ml(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) LMSmem<RP> sm;
-#define B_(d, b) lm_body<DT, RP, SA, SRC, WM, WE>(d, b, sm)
+#define B_(d, b) lm_body<DT, RP, SA, SRC, WM, WE, OUTBF>(d, b, sm)
   OCC_DISPATCH(K_MHAT, B_)
 #undef B_
 }
@@ -1814,7 +1822,7 @@ __device__ __forceinline__ void lmx_stage(const f4v* pr, uint16_t (*dst)[32 * (R
   }
 }
 
-template <int RP, int SRC, bool WM, bool WE>
+template <int RP, int SRC, bool WM, bool WE, bool OUTBF = false>
 __device__ __forceinline__ void lmx_body(const Desc& d, int b, LMXSmem<RP>& sm) {
   constexpr int NCT = lm_tiles(RP), KS = RP / 16, BC = lm_block_cols(RP);
   constexpr int SF = RP * 8 / kBlock;
@@ -1892,7 +1900,7 @@ __device__ __forceinline__ void lmx_body(const Desc& d, int b, LMXSmem<RP>& sm) 
         const int row = row0 + mf32_row(v, g);
         if (row < r_hi && col < d.n) {
           const float mh = acc[c][v];
-          if (WM) __builtin_nontemporal_store(mh, d.Mhat + (int64_t)row * d.ldh + col);
+          if (WM) store_mhat_nt<OUTBF>(d, (int64_t)row * d.ldh + col, mh);
           if (WE) {
             const float e = rawa_val<DT_F32, SA_SAVED, 1>(av[c][v], 0) - mh;
             __builtin_nontemporal_store(e, d.err_out + (int64_t)row * d.lde_out + col);
@@ -1905,10 +1913,10 @@ __device__ __forceinline__ void lmx_body(const Desc& d, int b, LMXSmem<RP>& sm) 
   }
 }
 
-template <int RP, int SRC, bool WM, bool WE>
+template <int RP, int SRC, bool WM, bool WE, bool OUTBF = false>
 __global__ __launch_bounds__(kBlock) void k_mlx(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) LMXSmem<RP> sm;
-#define B_(d, b) lmx_body<RP, SRC, WM, WE>(d, b, sm)
+#define B_(d, b) lmx_body<RP, SRC, WM, WE, OUTBF>(d, b, sm)
   OCC_DISPATCH(K_MHAT, B_)
 #undef B_
 }

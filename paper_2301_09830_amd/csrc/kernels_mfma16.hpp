@@ -559,7 +559,9 @@ __device__ __forceinline__ void factor_load(const float* base, int r, int row, b
   }
 }
 
-template <int DT, bool VEC, int RP, int SRC, bool WRITE_MHAT, bool WRITE_ERR>
+// OUTBF (stand-alone decompression only): M_hat is stored as bf16, each
+// element rounded to nearest even from the fp32 result.
+template <int DT, bool VEC, int RP, int SRC, bool WRITE_MHAT, bool WRITE_ERR, bool OUTBF = false>
 __device__ __forceinline__ void mh16_body(const Desc& d, int b, MXSmem& sm) {
   constexpr int S = RP / 4;        // MFMA K-steps (rank indices per lane group)
   constexpr int NTILE = F_MHCOLS / 16;
@@ -624,7 +626,11 @@ __device__ __forceinline__ void mh16_body(const Desc& d, int b, MXSmem& sm) {
         // streaming outputs: nontemporal stores (the dirty lines would
         // otherwise be written back during the next step's first pass)
         typedef float nt4 __attribute__((ext_vector_type(4)));
-        if (WRITE_MHAT)
+        typedef uint32_t nu2 __attribute__((ext_vector_type(2)));
+        if (WRITE_MHAT && OUTBF)
+          __builtin_nontemporal_store(nu2{bf16_pack2(mh[0], mh[1]), bf16_pack2(mh[2], mh[3])},
+                                      (nu2*)((uint16_t*)d.Mhat + (int64_t)row * d.ldh + col));
+        else if (WRITE_MHAT)
           __builtin_nontemporal_store(nt4{mh[0], mh[1], mh[2], mh[3]},
                                       (nt4*)(d.Mhat + (int64_t)row * d.ldh + col));
         if (WRITE_ERR)
@@ -634,7 +640,7 @@ __device__ __forceinline__ void mh16_body(const Desc& d, int b, MXSmem& sm) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           if (col + j < d.n) {
-            if (WRITE_MHAT) d.Mhat[(int64_t)row * d.ldh + col + j] = mh[j];
+            if (WRITE_MHAT) store_mhat1<OUTBF>(d, (int64_t)row * d.ldh + col + j, mh[j]);
             if (WRITE_ERR) d.err_out[(int64_t)row * d.lde_out + col + j] = e[j];
           }
         }
@@ -644,10 +650,10 @@ __device__ __forceinline__ void mh16_body(const Desc& d, int b, MXSmem& sm) {
   }
 }
 
-template <int DT, bool VEC, int RP, int SRC, bool WRITE_MHAT, bool WRITE_ERR>
+template <int DT, bool VEC, int RP, int SRC, bool WRITE_MHAT, bool WRITE_ERR, bool OUTBF = false>
 __global__ __launch_bounds__(kBlock) void k_mh16(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) MXSmem sm;
-#define B_(d, b) mh16_body<DT, VEC, RP, SRC, WRITE_MHAT, WRITE_ERR>(d, b, sm)
+#define B_(d, b) mh16_body<DT, VEC, RP, SRC, WRITE_MHAT, WRITE_ERR, OUTBF>(d, b, sm)
   OCC_DISPATCH(K_MHAT, B_)
 #undef B_
 }

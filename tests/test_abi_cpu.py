@@ -27,7 +27,7 @@ def test_exports_every_declared_symbol(L):
 
 
 def test_abi_version_and_status_strings(L):
-    assert optcc.occ_abi_version() == 1
+    assert optcc.occ_abi_version() == 2
     for code in range(11):
         assert optcc.occ_status_str(code)
     assert "unknown" in optcc.occ_status_str(99)
@@ -87,19 +87,38 @@ def test_batched_errors(L):
 
 def test_other_entry_points_validate(L):
     # decompress: rank > n
-    assert L.occ_decompress(1 << 20, 1 << 21, 10, 3, 4, 0, 1 << 22, 3, None) == 3
+    assert L.occ_decompress(1 << 20, 1 << 21, 10, 3, 4, 1 << 22, 3, None) == 3
     # decompress: output overlaps P
-    assert L.occ_decompress(1 << 20, 1 << 24, 10, 8, 4, 0, (1 << 20) + 8, 8, None) == 7
-    # decompress: unknown M dtype
-    assert L.occ_decompress(1 << 20, 1 << 24, 10, 8, 4, 2, 1 << 26, 8, None) == 5
-    # err_update: in place needs equal leading dimensions
-    assert L.occ_err_update(1 << 20, 0, 4, 4, 4, 1 << 24, 4, 1 << 26, 4, 1 << 24, 8, None) == 7
+    assert L.occ_decompress(1 << 20, 1 << 24, 10, 8, 4, (1 << 20) + 8, 8, None) == 7
+    # decompress_ex: unknown flag bit, bf16 output misaligned for its element size
+    assert L.occ_decompress_ex(1 << 20, 1 << 24, 10, 8, 4, 4, 1 << 26, 8, None) == 10
+    assert L.occ_decompress_ex(1 << 20, 1 << 24, 10, 8, 4, 2, (1 << 26) + 1, 8, None) == 6
+    # decompress_ex: a bf16 M_hat of 10 x 8 at ld 8 spans 160 bytes; a P 100
+    # bytes after its start overlaps it
+    assert L.occ_decompress_ex((1 << 26) + 100, 1 << 24, 10, 8, 4, 2, 1 << 26, 8, None) == 7
+    # err_update: err_new overlapping M
+    assert L.occ_err_update(1 << 20, 0, 4, 4, 4, 1 << 24, 4, 1 << 26, 4, (1 << 20) + 4,
+                            None) == 7
+    # err_update: unknown dtype, leading dimension below cols
+    assert L.occ_err_update(1 << 20, 3, 4, 4, 4, 1 << 24, 4, 1 << 26, 4, 1 << 24, None) == 5
+    assert L.occ_err_update(1 << 20, 0, 4, 4, 4, 1 << 24, 3, 1 << 26, 4, 1 << 24, None) == 2
     # compress: missing workspace
     assert L.occ_compress(1 << 20, 0, 16, 16, 16, None, 0, 1 << 24, 1 << 26, 2, 1, None, 0,
                           None) == 8
     assert L.occ_workspace_init(None, 1024, None) == 1
     flags = ctypes.c_uint32()
     assert L.occ_get_flags(None, ctypes.byref(flags), 0, None) == 1
+
+
+def test_compress_workspace_follows_dtype(L):
+    """The compress-only workspace is sized for the M dtype it will run on
+    (the large-rank tiling depends on it); an unknown dtype gives 0."""
+    for dt in (optcc.OCC_F32, optcc.OCC_BF16):
+        a = L.occ_compress_workspace_bytes(8192, 4096, dt, 128, 2)
+        arr = (optcc.occ_mat_t * 1)()
+        arr[0].rows, arr[0].cols, arr[0].ldm, arr[0].m_dtype = 8192, 4096, 4096, dt
+        assert a > 0 and a == L.occ_workspace_bytes(arr, 1, 128, 2)
+    assert L.occ_compress_workspace_bytes(8192, 4096, 5, 16, 1) == 0
 
 
 def test_workspace_size_is_deterministic_and_grows(L):

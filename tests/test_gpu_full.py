@@ -2,43 +2,54 @@
 bench.py times (one occ_step_batched call per step over all matrices of the
 workload, error buffer and Q carried from step to step).
 
-Every matrix of a step is checked against the invariants that hold at any
-size (M_hat + err == A, orthonormal P_hat, residual orthogonal to P_hat);
-the float64 oracle follows every matrix of the single-matrix workloads and a
-sample of the batched ones (one matrix of each shape), along its own
-trajectory.  Tolerances as in test_gpu_parity.py.  The 1024 x 1024 workload
-runs at full size there.
+Every matrix of every step is checked against the invariants that hold at
+any size (M_hat + err == A, orthonormal P_hat, residual orthogonal to P_hat)
+and against the float64 oracle along its own trajectory: the graded relative
+Frobenius error, the same tolerance per row and per 128-column tile, and the
+regression bounds of gpu_util.  The high-SNR diagnostics (signal scaled to
+unit-RMS entries over 1 % noise, so that err is about 1 % of A) run at full
+size as well; their widths are multiples of 32, so they take the LDS-tile
+paths of the left and right products like the graded inputs.  The 1024 x 1024
+workload runs at full size in test_gpu_parity.py.
 """
 
 import pytest
 
 from gpu_util import assert_parity, run_workload
-from workloads import WORKLOADS
+from workloads import WORKLOADS, high_snr
 
 pytestmark = pytest.mark.gpu
 
 
-def _run(key, oracle_mats=None):
-    w = WORKLOADS[key]
+def _run(w, steps=None, **bounds):
+    steps = w.steps if steps is None else steps
     print(f"[full] {w.name}: {len(w.shapes)} matrices, rank {w.rank}, iters {w.iters}, "
-          f"{w.steps} steps", flush=True)
-    res, _, _ = run_workload(w, w.steps, batched=True, oracle_mats=oracle_mats,
-                             invariants_all=True)
-    assert_parity(res, w.m_dtype, w.name)
+          f"{steps} steps", flush=True)
+    res, _, _ = run_workload(w, steps, batched=True, invariants_all=True)
+    assert_parity(res, w.m_dtype, w.name, **bounds)
 
 
 def test_full_act_grad_8192x4096_bf16_r16_8_steps():
-    _run(2)
+    _run(WORKLOADS[2])
+
+
+def test_full_act_grad_8192x4096_high_snr():
+    # err is about 1 % of A here, so its relative error is about 100 times
+    # that of M_hat: looser regression bounds (graded tolerance unchanged)
+    _run(high_snr(WORKLOADS[2]), steps=3, reg_rel=5e-4, reg_loc=5e-3)
 
 
 def test_full_stage_weights_36_matrices_f32_r32_t2():
-    # layer 0 and layer 8 of each of the four shapes
-    _run(3, oracle_mats=[0, 1, 2, 3, 32, 33, 34, 35])
+    _run(WORKLOADS[3])
 
 
 def test_full_embedding_51200x3072_zipf_f32_r64():
-    _run(4)
+    _run(WORKLOADS[4])
 
 
 def test_full_act_grad_4x16384x8192_bf16_r128_t2():
-    _run(5, oracle_mats=[0, 3])
+    _run(WORKLOADS[5])
+
+
+def test_full_act_grad_4x16384x8192_high_snr():
+    _run(high_snr(WORKLOADS[5]), reg_rel=5e-4, reg_loc=5e-3)

@@ -29,7 +29,17 @@ def test_config2_ragged_multistep():
 def test_config2_high_snr_ragged():
     w = high_snr(WORKLOADS[2].scaled([(777, 520)]))
     res, _, _ = run_workload(w, 3)
-    assert_parity(res, "bf16", "act_grad high-SNR 777x520")
+    assert_parity(res, "bf16", "act_grad high-SNR 777x520", reg_rel=5e-4, reg_loc=5e-3)
+
+
+@pytest.mark.parametrize("shape", [(1000, 512), (1000, 4096)])
+def test_config2_high_snr_lds_tiles(shape):
+    """High-SNR recipe at widths that are multiples of 32: the rank-16 left
+    product takes its LDS-tile path, as on the full-size input."""
+    w = high_snr(WORKLOADS[2].scaled([shape]))
+    res, _, _ = run_workload(w, 3)
+    assert_parity(res, "bf16", f"act_grad high-SNR {shape[0]}x{shape[1]} (LDS tiles)",
+                  reg_rel=5e-4, reg_loc=5e-3)
 
 
 @pytest.mark.parametrize("rank", [1, 3, 4, 8, 16, 17, 32, 64, 100, 128])
@@ -108,17 +118,23 @@ def test_config5_batched_small():
     assert_parity(res, "bf16", "act_grad 2x700x520 r128 t2 batched")
 
 
-def test_config5_high_snr_small():
-    w = high_snr(WORKLOADS[5].scaled([(700, 520)], signal_rank=160))
+@pytest.mark.parametrize("shape", [(700, 520), (700, 512)])
+def test_config5_high_snr_small(shape):
+    """High-SNR rank-128 recipe; 512 columns take the LDS-tile paths."""
+    w = high_snr(WORKLOADS[5].scaled([shape], signal_rank=160))
     res, _, _ = run_workload(w, 2)
-    assert_parity(res, "bf16", "act_grad high-SNR 700x520 r128 t2")
+    assert_parity(res, "bf16", f"act_grad high-SNR {shape[0]}x{shape[1]} r128 t2",
+                  reg_rel=5e-4, reg_loc=5e-3)
 
 
-@pytest.mark.parametrize("rank,iters,ratio", [(8, 2, 1.5), (16, 2, 1.2), (12, 3, 1.2), (32, 2, 1.1)])
+@pytest.mark.parametrize("rank,iters,ratio", [(8, 2, 1.5), (16, 2, 1.2), (12, 3, 1.2), (32, 2, 1.1),
+                                              (64, 2, 1.05), (128, 2, 1.025)])
 def test_ill_conditioned_iterates_second_pass(rank, iters, ratio):
     """Geometric spectrum ratio^-j: the power iterates P have condition
-    number ratio^((2t-1)(r-1)) between 1e3 and 1e5, so the Cholesky diagonal
-    spans more than 1e3 and the CholeskyQR second pass runs.  (Much larger
+    number ratio^((2t-1)(r-1)) between 1e3 and 1e5 (1.05^189 = 1.0e4 at rank
+    64, 1.025^381 = 1.2e4 at rank 128), so the Cholesky diagonal spans more
+    than 1e3 and the CholeskyQR second pass runs, on the small-rank kernel up
+    to rank 16 and on the blocked fp64 Cholesky above.  (Much larger
     condition numbers exceed what an fp32 P can resolve.)  The recipe's
     "noise" field carries the ratio."""
     w = Workload(93, "geom", ((400, 300),), "f32", rank, iters, 2, "geom",
