@@ -358,6 +358,9 @@ def main() -> int:
     ap.add_argument("--workload", type=int, default=2, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--inputs", type=int, default=0,
                     help="distinct seeded inputs cycled through (default: the workload's steps)")
+    ap.add_argument("--rows", action="store_true",
+                    help="embedding workload: the row-sparse step over the union of the "
+                         "inputs' nonzero rows (bytes accounted by rows touched)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--cold-reps", type=int, default=30,
@@ -412,17 +415,42 @@ def main() -> int:
             mat = optcc.make_mat(dev_M[(s, j)], errs[j], Ps[j], Qs[j], Mhs[j])
             arr[j] = mat
         arrays.append(arr)
-    ws_bytes = L.occ_workspace_bytes(arrays[0], count, w.rank, w.iters)
+    n_live = None
+    if args.rows:
+        # Row-sparse step: one list for every timed step, the union of the
+        # nonzero rows of all the inputs cycled through (the carried error
+        # stays inside it: its rows are those of earlier inputs).
+        if w.kind != "zipf" or count != 1:
+            raise SystemExit("--rows applies to the embedding workload (--workload 4)")
+        live = np.zeros(w.shapes[0][0], dtype=bool)
+        for v in host.values():
+            live |= (v != 0).any(axis=1)
+        rows_t = torch.from_numpy(np.nonzero(live)[0].astype(np.int32)).cuda()
+        n_live = int(rows_t.numel())
+        Ps = [torch.empty((n_live, w.rank), dtype=torch.float32, device="cuda")]
+        Mhs = [torch.zeros(w.shapes[0], dtype=torch.float32, device="cuda")]
+        for s in range(n_inputs):
+            arrays[s][0].P = Ps[0].data_ptr()
+            arrays[s][0].M_hat = Mhs[0].data_ptr()
+        dt_code = optcc.OCC_BF16 if w.m_dtype == "bf16" else optcc.OCC_F32
+        ws_bytes = L.occ_step_rows_workspace_bytes(n_live, w.shapes[0][1], dt_code, w.rank,
+                                                   w.iters)
+    else:
+        ws_bytes = L.occ_workspace_bytes(arrays[0], count, w.rank, w.iters)
     ws = optcc.alloc_workspace(ws_bytes)
     stream = torch.cuda.current_stream()
     sptr = int(stream.cuda_stream)
     wsp = int(ws.data_ptr())
 
     def step(k: int) -> None:
-        st = L.occ_step_batched(arrays[k % n_inputs], count, w.rank, w.iters, 0, wsp, ws_bytes,
-                                sptr)
+        if n_live is not None:
+            st = L.occ_step_rows(arrays[k % n_inputs], int(rows_t.data_ptr()), n_live, w.rank,
+                                 w.iters, 0, wsp, ws_bytes, sptr)
+        else:
+            st = L.occ_step_batched(arrays[k % n_inputs], count, w.rank, w.iters, 0, wsp,
+                                    ws_bytes, sptr)
         if st != 0:
-            raise optcc.OccError("occ_step_batched", st)
+            raise optcc.OccError("occ_step_rows" if n_live is not None else "occ_step_batched", st)
 
     for k in range(args.warmup):
         step(k)
@@ -440,9 +468,11 @@ def main() -> int:
     ms_events = ev0.elapsed_time(ev1)
     ms_per_step = ms_events / args.steps
 
-    elements = w.elements
+    wname = w.name + ("_rows" if n_live is not None else "")
+    # bytes accounted by the rows the step touches (all rows unless --rows)
+    elements = w.elements if n_live is None else n_live * w.shapes[0][1]
     m_bytes = 2 if w.m_dtype == "bf16" else 4
-    input_bytes = w.m_bytes
+    input_bytes = elements * m_bytes
     value = input_bytes / (ms_per_step * 1e-3) / 1e9
     step_bytes = step_alg_bytes(elements, m_bytes, w.iters)
 
@@ -496,7 +526,7 @@ def main() -> int:
             avg_s = total_ms / launches * 1e-3
             per_launch = kernel_alg_bytes(dom, elements, m_bytes)  # one launch covers the batch
             flops = kernel_alg_flops(dom, elements, w.rank)
-            prof_rec = load_profile(dom, w.name)
+            prof_rec = load_profile(dom, wname)
             traffic = None if prof_rec is None else prof_rec.get("hbm_bytes_per_launch")
             # the bound is whichever resource the kernel's algorithmic work
             # needs longer on: HBM bytes at 8 TB/s or its flops on the matrix
@@ -550,9 +580,12 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": w.name, "shapes": [list(s) for s in w.shapes],
+        "config": {"workload": wname,
+                   "shapes": [list(s) for s in w.shapes],
                    "m_dtype": w.m_dtype, "rank": w.rank, "iters": w.iters,
-                   "distinct_inputs": n_inputs, "state": "err and Q carried across steps"},
+                   "distinct_inputs": n_inputs, "state": "err and Q carried across steps",
+                   **({"live_rows": n_live, "live_fraction": round(n_live / w.shapes[0][0], 4),
+                       "entry_point": "occ_step_rows"} if n_live is not None else {})},
         "step_roofline": {"alg_bytes_per_step": step_bytes,
                           "achieved": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
                           "frac": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),

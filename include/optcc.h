@@ -75,8 +75,11 @@ typedef enum {
 
 typedef enum { OCC_F32 = 0, OCC_BF16 = 1 } occ_dtype_t;
 
-/* sticky numeric flags, read with occ_get_flags */
-enum { OCC_F_NONFINITE = 1u, OCC_F_RANK_DEFICIENT = 2u };
+/* sticky numeric flags, read with occ_get_flags; OCC_F_BAD_ROWS: the row list
+ * of occ_step_rows was not strictly increasing inside [0, rows) (the results
+ * of that call are then unspecified, but no memory outside the arguments is
+ * touched) */
+enum { OCC_F_NONFINITE = 1u, OCC_F_RANK_DEFICIENT = 2u, OCC_F_BAD_ROWS = 4u };
 
 /* call flags for occ_step / occ_step_batched */
 enum { OCC_NO_MHAT = 1u }; /* sender side: do not write M_hat (err is still updated) */
@@ -182,6 +185,69 @@ occ_status_t occ_step(const occ_mat_t* mat, int rank, int iters, unsigned flags,
 occ_status_t occ_step_batched(const occ_mat_t* mats, int count, int rank, int iters,
                               unsigned flags, void* ws, size_t ws_bytes,
                               occ_stream_t stream);
+
+/* Row-sparse step for embedding gradients.  The first pipeline stage's copy
+ * of the embedding converts the batch's words into embedding values (Sec. 6),
+ * so the gradient of that lookup is zero outside the rows of the words the
+ * batch contains.  `rows` (DEVICE pointer, n_rows int32 entries, strictly
+ * increasing, each in [0, mat->rows)) lists the rows to compress; the call
+ * compresses the n_rows x cols matrix of those rows of M + err and reads and
+ * writes nothing else of M, err and M_hat: every other row of err and M_hat
+ * is left untouched.  When M and err are zero outside the listed rows (the
+ * list is the union of the nonzero rows of both), the result equals
+ * occ_step on the whole matrix with M_hat zero in the unlisted rows.
+ *   mat->P   receives P_hat in compact form: n_rows x rank, row i belonging to
+ *            matrix row rows[i];
+ *   mat->Q   warm start in, A^T P_hat out (cols x rank), as in occ_step.
+ * Requires n_rows >= rank, except n_rows == 0 (then A is zero: Q is set to
+ * zero and OCC_F_RANK_DEFICIENT raised); a caller with fewer live rows than
+ * `rank` can list additional zero rows.  The list is checked on the device:
+ * a violation raises OCC_F_BAD_ROWS.  Workspace: occ_step_rows_workspace_bytes. */
+occ_status_t occ_step_rows(const occ_mat_t* mat, const int32_t* rows, int64_t n_rows, int rank,
+                           int iters, unsigned flags, void* ws, size_t ws_bytes,
+                           occ_stream_t stream);
+
+/* Workspace bytes occ_step_rows needs for n_rows listed rows of a matrix with
+ * `cols` columns and M dtype m_dtype.  Returns 0 for invalid arguments. */
+size_t occ_step_rows_workspace_bytes(int64_t n_rows, int64_t cols, int m_dtype, int rank,
+                                     int iters);
+
+/* Selective stage compression (Sec. 7), host-side model.  With pipeline
+ * parallelism the later stages finish their backward passes first and start
+ * their data-parallel gradient exchange early; the exchange of the earliest
+ * stage is left exposed.  Compressing the exchanges of chosen stages,
+ * starting from the earliest, trades compression error for time; each choice
+ * moves the bottleneck to another stage.  Times are in one unit of the
+ * caller's choice; no device is touched. */
+
+/* When each stage's last backward pass ends under the one-forward-one-
+ * backward pipeline schedule (Sec. 2.2), by event simulation: n_stages
+ * uniform stages, n_micro micro-batches, t_fwd / t_bwd per micro-batch and
+ * stage, t_p2p per hop between adjacent stages.  bwd_done receives n_stages
+ * values; *t_end (if not NULL) the end of the schedule.  Invalid counts or
+ * negative / non-finite times return OCC_E_SHAPE. */
+occ_status_t occ_pipeline_1f1b(int n_stages, int n_micro, double t_fwd, double t_bwd,
+                               double t_p2p, double* bwd_done, double* t_end);
+
+/* One stage for occ_sc_select. */
+typedef struct {
+  double bwd_done;        /* end of the stage's last backward pass */
+  double comm;            /* its data-parallel gradient exchange, uncompressed */
+  double comm_compressed; /* the exchange of the low-rank factors instead */
+  double compress;        /* compressor time on the stage's gradients (e.g. a
+                             measured occ_step_batched over the stage) */
+} occ_stage_t;
+
+/* Chooses the stages to compress: the exchange of stage s ends at
+ * bwd_done + comm, or bwd_done + compress + comm_compressed when compressed.
+ * Starting with none compressed, while fewer than max_compressed are, the
+ * stage whose exchange ends last is compressed if that ends it earlier; the
+ * selection stops at the first bottleneck that is compressed already or would
+ * not gain.  selected[s] = 1 for a chosen stage, else 0; *n_selected (if not
+ * NULL) the count; *t_end (if not NULL) the end of the last exchange, the
+ * least that any choice of at most max_compressed stages reaches. */
+occ_status_t occ_sc_select(const occ_stage_t* stages, int n_stages, int max_compressed,
+                           uint8_t* selected, int* n_selected, double* t_end);
 
 /* Read (and optionally clear) the sticky numeric flags of a workspace.
  * Synchronises `stream`. */

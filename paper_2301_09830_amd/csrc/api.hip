@@ -20,6 +20,7 @@
 #include "kernels_small.hpp"
 #include "kernels_mfma16.hpp"
 #include "kernels_large.hpp"
+#include "sc_model.hpp"
 
 using namespace occ;
 
@@ -362,8 +363,12 @@ occ_status_t plan_batch(const occ_mat_t* mats, int count, int rank, int iters, u
 unsigned grid_of(int64_t blocks) { return (unsigned)std::max<int64_t>(blocks, 1); }
 
 // Enqueue the compression passes (and, with `finish`, the fused
-// reconstruction/residual pass) for a planned batch.
-occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, hipStream_t s) {
+// reconstruction/residual pass) for a planned batch; numeric flags go to
+// `flags`.  RM: row-sparse step (rows of M, err and M_hat through each
+// descriptor's row map), on the register-load forms of the streaming kernels.
+template <bool RM>
+occ_status_t run_batch_t(const Batch& b, void* ws, uint32_t* flags, bool finish, bool write_mhat,
+                         hipStream_t s) {
   const int count = (int)b.descs.size();
   const Desc* table = nullptr;
   Desc single = b.descs[0];
@@ -379,7 +384,6 @@ occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, h
       }));
     }
   }
-  uint32_t* flags = (uint32_t*)ws;
   const dim3 blk(kBlock);
   occ_status_t st = OCC_OK;
   with_rp(b.rp, [&](auto RPc) {
@@ -401,16 +405,16 @@ occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, h
         if (b.fused) {
           if (b.descs[0].r != RP) L("qpad", k_qpad<RP>, b.blocks[K_QPAD]);
           for (int it = 0; it < b.iters; ++it) {
-            LB("pass_p", k_pm<DT, VEC, RP>, b.blocks[K_PASS_P], PM_THREADS);
+            LB("pass_p", k_pm<DT, VEC, RP, RM>, b.blocks[K_PASS_P], PM_THREADS);
             LB("orth", k_orth16<RP>, b.blocks[K_PGRAM], CH_THREADS, flags);
-            LB("pass_q", k_qm<DT, VEC, RP>, b.blocks[K_PASS_Q], QM_THREADS);
+            LB("pass_q", k_qm<DT, VEC, RP, RM>, b.blocks[K_PASS_Q], QM_THREADS);
             L("q_reduce", k_qred16<RP>, b.blocks[K_QRED]);
           }
           if (finish) {
             if (write_mhat)
-              L("mhat_err", k_mh16<DT, VEC, RP, 0, true, true>, b.blocks[K_MHAT]);
+              L("mhat_err", k_mh16<DT, VEC, RP, 0, true, true, false, RM>, b.blocks[K_MHAT]);
             else
-              L("err_only", k_mh16<DT, VEC, RP, 0, false, true>, b.blocks[K_MHAT]);
+              L("err_only", k_mh16<DT, VEC, RP, 0, false, true, false, RM>, b.blocks[K_MHAT]);
           }
           return;
         }
@@ -424,26 +428,28 @@ occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, h
         constexpr bool X3 = DT == DT_BF16;
         // left products with their A tiles through LDS when every row is
         // 16-byte aligned, every 32-column K-step whole and A has a source
-        bool whole = VEC;
+        // (never with a row map: TL instances are the register forms then)
+        constexpr bool TL = !RM;
+        bool whole = VEC && TL;
         for (const Desc& dd : b.descs) whole = whole && dd.n % 32 == 0;
         const bool tiles_merr = whole && b.descs[0].err_in != nullptr;
         L("qpad", k_qpadl<RP>, b.blocks[K_QPAD]);
         for (int it = 0; it < b.iters; ++it) {
           if (!saved) {
             if (tiles_merr)
-              L("pass_p", k_lp<DT, RP, SA_MERR, X3, true>, b.blocks[K_PASS_P]);
+              L("pass_p", k_lp<DT, RP, SA_MERR, X3, TL, RM>, b.blocks[K_PASS_P]);
             else
-              L("pass_p", k_lp<DT, RP, SA_MERR, X3, false>, b.blocks[K_PASS_P]);
+              L("pass_p", k_lp<DT, RP, SA_MERR, X3, false, RM>, b.blocks[K_PASS_P]);
           } else if (it == 0) {
             if (tiles_merr)
-              L("pass_p_first", k_lp<DT, RP, SA_MERR_SAVE, X3, true>, b.blocks[K_PASS_P]);
+              L("pass_p_first", k_lp<DT, RP, SA_MERR_SAVE, X3, TL, RM>, b.blocks[K_PASS_P]);
             else
-              L("pass_p_first", k_lp<DT, RP, SA_MERR_SAVE, X3, false>, b.blocks[K_PASS_P]);
+              L("pass_p_first", k_lp<DT, RP, SA_MERR_SAVE, X3, false, RM>, b.blocks[K_PASS_P]);
           } else {
             if (whole)
-              L("pass_p_a", k_lp<DT_F32, RP, SA_SAVED, X3, true>, b.blocks[K_PASS_P]);
+              L("pass_p_a", k_lp<DT_F32, RP, SA_SAVED, X3, TL, RM>, b.blocks[K_PASS_P]);
             else
-              L("pass_p_a", k_lp<DT_F32, RP, SA_SAVED, X3, false>, b.blocks[K_PASS_P]);
+              L("pass_p_a", k_lp<DT_F32, RP, SA_SAVED, X3, false, RM>, b.blocks[K_PASS_P]);
           }
           L("gram", k_lg<RP, 0>, b.blocks[K_PGRAM]);
           L("gram_sum", k_gsum<RP, 0>, b.blocks[K_GSUM]);
@@ -456,18 +462,18 @@ occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, h
           if constexpr (X3) {
             // the stored A through LDS tiles under the same conditions
             if (saved && whole)
-              L("pass_q_a", k_lqx<DT_F32, RP, SA_SAVED, true>, b.blocks[K_PASS_Q]);
+              L("pass_q_a", k_lqx<DT_F32, RP, SA_SAVED, TL, RM>, b.blocks[K_PASS_Q]);
             else if (saved)
-              L("pass_q_a", k_lqx<DT_F32, RP, SA_SAVED, false>, b.blocks[K_PASS_Q]);
+              L("pass_q_a", k_lqx<DT_F32, RP, SA_SAVED, false, RM>, b.blocks[K_PASS_Q]);
             else
-              L("pass_q", k_lqx<DT, RP, SA_MERR, false>, b.blocks[K_PASS_Q]);
+              L("pass_q", k_lqx<DT, RP, SA_MERR, false, RM>, b.blocks[K_PASS_Q]);
           } else {
             if (saved && whole)
-              L("pass_q_a", k_lq<DT_F32, RP, SA_SAVED, true>, b.blocks[K_PASS_Q]);
+              L("pass_q_a", k_lq<DT_F32, RP, SA_SAVED, TL, RM>, b.blocks[K_PASS_Q]);
             else if (saved)
-              L("pass_q_a", k_lq<DT_F32, RP, SA_SAVED, false>, b.blocks[K_PASS_Q]);
+              L("pass_q_a", k_lq<DT_F32, RP, SA_SAVED, false, RM>, b.blocks[K_PASS_Q]);
             else
-              L("pass_q", k_lq<DT, RP, SA_MERR, false>, b.blocks[K_PASS_Q]);
+              L("pass_q", k_lq<DT, RP, SA_MERR, false, RM>, b.blocks[K_PASS_Q]);
           }
           L("q_reduce", k_qredl<RP>, b.blocks[K_QRED]);
         }
@@ -475,20 +481,26 @@ occ_status_t run_batch(const Batch& b, void* ws, bool finish, bool write_mhat, h
           // bf16 M: the reconstruction on bf16 matrix cores with split operands
           if constexpr (X3) {
             if (write_mhat)
-              L("mhat_err_a", k_mlx<RP, 0, true, true>, b.blocks[K_MHAT]);
+              L("mhat_err_a", k_mlx<RP, 0, true, true, false, RM>, b.blocks[K_MHAT]);
             else
-              L("err_only_a", k_mlx<RP, 0, false, true>, b.blocks[K_MHAT]);
+              L("err_only_a", k_mlx<RP, 0, false, true, false, RM>, b.blocks[K_MHAT]);
           } else {
             if (write_mhat)
-              L("mhat_err_a", k_ml<DT_F32, RP, SA_SAVED, 0, true, true>, b.blocks[K_MHAT]);
+              L("mhat_err_a", k_ml<DT_F32, RP, SA_SAVED, 0, true, true, false, RM>, b.blocks[K_MHAT]);
             else
-              L("err_only_a", k_ml<DT_F32, RP, SA_SAVED, 0, false, true>, b.blocks[K_MHAT]);
+              L("err_only_a", k_ml<DT_F32, RP, SA_SAVED, 0, false, true, false, RM>, b.blocks[K_MHAT]);
           }
         }
       }
     });
   });
   return st;
+}
+
+occ_status_t run_batch(const Batch& b, void* ws, uint32_t* flags, bool finish, bool write_mhat,
+                       hipStream_t s) {
+  return b.descs[0].rmap ? run_batch_t<true>(b, ws, flags, finish, write_mhat, s)
+                         : run_batch_t<false>(b, ws, flags, finish, write_mhat, s);
 }
 
 }  // namespace
@@ -548,6 +560,36 @@ occ_status_t decompress_impl(const float* P, const float* Q, int64_t m, int64_t 
 
 }  // namespace
 
+namespace {
+
+// Plan of a row-sparse step: the compressed matrix is the n_rows x cols
+// matrix of the listed rows; its workspace regions are those of a dense
+// matrix of that shape, followed by the validated copy of the row list.
+occ_status_t plan_rows(const occ_mat_t* mat, int64_t n_rows, int rank, int iters, unsigned flags,
+                       Batch& b, size_t& rows_off) {
+  if (!mat) return OCC_E_NULL;
+  if (flags & ~(unsigned)OCC_NO_MHAT) return OCC_E_FLAGS;
+  if (mat->m_dtype != OCC_F32 && mat->m_dtype != OCC_BF16) return OCC_E_DTYPE;
+  OCC_TRY(check_shape(mat->rows, mat->cols, mat->ldm));
+  if (n_rows < 0 || n_rows > mat->rows) return OCC_E_SHAPE;
+  if (n_rows == 0) {
+    if (rank < 1 || rank > OCC_MAX_RANK || rank > mat->cols) return OCC_E_RANK;
+    if (iters < 1 || iters > OCC_MAX_ITERS) return OCC_E_ITERS;
+    b = Batch{};
+    b.ws_needed = kHeaderBytes;
+    rows_off = 0;
+    return OCC_OK;
+  }
+  occ_mat_t a = *mat;
+  a.rows = n_rows;
+  OCC_TRY(plan_batch(&a, 1, rank, iters, flags, nullptr, 0, true, b));
+  rows_off = b.ws_needed;
+  b.ws_needed += align_up((size_t)n_rows * 4);
+  return OCC_OK;
+}
+
+}  // namespace
+
 // ============================================================================
 // C ABI
 // ============================================================================
@@ -601,13 +643,89 @@ occ_status_t occ_step_batched(const occ_mat_t* mats, int count, int rank, int it
                               unsigned flags, void* ws, size_t ws_bytes, occ_stream_t stream) {
   Batch b;
   OCC_TRY(plan_batch(mats, count, rank, iters, flags, ws, ws_bytes, false, b));
-  return run_batch(b, ws, true, !(flags & OCC_NO_MHAT), (hipStream_t)stream);
+  return run_batch(b, ws, (uint32_t*)ws, true, !(flags & OCC_NO_MHAT), (hipStream_t)stream);
 }
 
 occ_status_t occ_step(const occ_mat_t* mat, int rank, int iters, unsigned flags, void* ws,
                       size_t ws_bytes, occ_stream_t stream) {
   if (!mat) return OCC_E_NULL;
   return occ_step_batched(mat, 1, rank, iters, flags, ws, ws_bytes, stream);
+}
+
+size_t occ_step_rows_workspace_bytes(int64_t n_rows, int64_t cols, int m_dtype, int rank,
+                                     int iters) {
+  occ_mat_t a{};
+  a.rows = std::max<int64_t>(n_rows, 1);
+  a.cols = cols;
+  a.ldm = cols;
+  a.m_dtype = m_dtype;
+  Batch b;
+  size_t rows_off = 0;
+  if (plan_rows(&a, n_rows, rank, iters, 0, b, rows_off) != OCC_OK) return 0;
+  return b.ws_needed;
+}
+
+occ_status_t occ_step_rows(const occ_mat_t* mat, const int32_t* rows, int64_t n_rows, int rank,
+                           int iters, unsigned flags, void* ws, size_t ws_bytes,
+                           occ_stream_t stream) {
+  Batch b;
+  size_t rows_off = 0;
+  OCC_TRY(plan_rows(mat, n_rows, rank, iters, flags, b, rows_off));
+  const occ_mat_t& a = *mat;
+  const bool write_mhat = !(flags & OCC_NO_MHAT);
+  OCC_TRY(check_shape(a.rows, a.cols, a.lde));
+  if (write_mhat) OCC_TRY(check_shape(a.rows, a.cols, a.ldh));
+  if (!a.M || !a.err || !a.Q || (n_rows > 0 && (!a.P || !rows)) || (write_mhat && !a.M_hat))
+    return OCC_E_NULL;
+  if (!ws) return OCC_E_WORKSPACE;
+  if (!aligned(ws, kAlign) || ws_bytes < b.ws_needed) return OCC_E_WORKSPACE;
+  const int dt = a.m_dtype;
+  const size_t es = elem_size(dt);
+  if (!aligned(a.M, es) || !aligned(a.err, 4) || !aligned(a.Q, 4) || (a.P && !aligned(a.P, 4)) ||
+      (rows && !aligned(rows, 4)) || (write_mhat && !aligned(a.M_hat, 4)))
+    return OCC_E_ALIGN;
+  std::vector<Span> spans = {span2d(a.M, a.rows, a.cols, a.ldm, es, false),
+                             span2d(a.err, a.rows, a.cols, a.lde, 4, true),
+                             span2d(a.Q, a.cols, rank, rank, 4, true),
+                             {(uintptr_t)ws, (uintptr_t)ws + b.ws_needed, true}};
+  if (n_rows > 0) {
+    spans.push_back(span2d(a.P, n_rows, rank, rank, 4, true));
+    spans.push_back(span2d(rows, 1, n_rows, n_rows, 4, false));
+  }
+  if (write_mhat) spans.push_back(span2d(a.M_hat, a.rows, a.cols, a.ldh, 4, true));
+  if (overlaps(spans)) return OCC_E_ALIAS;
+  hipStream_t s = (hipStream_t)stream;
+  uint32_t* fl = (uint32_t*)ws;
+  if (n_rows == 0) {
+    const int64_t nq = a.cols * rank;
+    return launch("rows_empty", s, [&] {
+      hipLaunchKernelGGL(k_rows_empty, dim3((unsigned)std::min<int64_t>(cdiv(nq, kBlock), 1024)),
+                         dim3(kBlock), 0, s, a.Q, nq, fl);
+    });
+  }
+  int32_t* rmap = (int32_t*)((char*)ws + rows_off);
+  OCC_TRY(launch("rows_check", s, [&] {
+    hipLaunchKernelGGL(k_rows_check, dim3((unsigned)std::min<int64_t>(cdiv(n_rows, kBlock), 1024)),
+                       dim3(kBlock), 0, s, rows, n_rows, (int32_t)a.rows, rmap, fl);
+  }));
+  finalize_regions(b, ws);
+  Desc& d = b.descs[0];
+  if (dt != OCC_BF16) d.qbf = nullptr;
+  d.M = a.M;
+  d.err_in = a.err;
+  d.err_out = a.err;
+  d.P = a.P;
+  d.Q = a.Q;
+  d.Mhat = write_mhat ? a.M_hat : nullptr;
+  d.ldm = (int32_t)a.ldm;
+  d.lde_in = (int32_t)a.lde;
+  d.lde_out = (int32_t)a.lde;
+  d.ldh = write_mhat ? (int32_t)a.ldh : 0;
+  d.rmap = rmap;
+  b.vec = aligned(a.M, 16) && a.ldm % (dt == OCC_BF16 ? 8 : 4) == 0 && aligned(a.err, 16) &&
+          a.lde % 4 == 0 && (!write_mhat || (aligned(a.M_hat, 16) && a.ldh % 4 == 0));
+  d.vec = b.vec ? 1 : 0;
+  return run_batch(b, ws, fl, true, write_mhat, s);
 }
 
 occ_status_t occ_compress(const void* M, int m_dtype, int64_t m, int64_t n, int64_t ldm,
@@ -653,7 +771,7 @@ occ_status_t occ_compress(const void* M, int m_dtype, int64_t m, int64_t n, int6
   b.vec = aligned(M, 16) && ldm % (m_dtype == OCC_BF16 ? 8 : 4) == 0 &&
           (!err_prev || (aligned(err_prev, 16) && lde % 4 == 0));
   d.vec = b.vec ? 1 : 0;
-  return run_batch(b, ws, false, false, (hipStream_t)stream);
+  return run_batch(b, ws, (uint32_t*)ws, false, false, (hipStream_t)stream);
 }
 
 occ_status_t occ_decompress(const float* P, const float* Q, int64_t m, int64_t n, int rank,
@@ -723,6 +841,32 @@ occ_status_t occ_get_flags(void* ws, uint32_t* flags_out, int clear, occ_stream_
       hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(64), 0, s, (uint32_t*)ws, 1);
     });
   }
+  return OCC_OK;
+}
+
+occ_status_t occ_pipeline_1f1b(int n_stages, int n_micro, double t_fwd, double t_bwd,
+                               double t_p2p, double* bwd_done, double* t_end) {
+  if (!bwd_done) return OCC_E_NULL;
+  if (n_stages < 1 || n_micro < 1 || n_stages > 4096 || n_micro > (1 << 20)) return OCC_E_SHAPE;
+  for (double t : {t_fwd, t_bwd, t_p2p})
+    if (!(t >= 0.0) || !std::isfinite(t)) return OCC_E_SHAPE;
+  return pipeline_1f1b(n_stages, n_micro, t_fwd, t_bwd, t_p2p, bwd_done, t_end) ? OCC_OK
+                                                                               : OCC_E_SHAPE;
+}
+
+occ_status_t occ_sc_select(const occ_stage_t* stages, int n_stages, int max_compressed,
+                           uint8_t* selected, int* n_selected, double* t_end) {
+  if (!stages || !selected) return OCC_E_NULL;
+  if (n_stages < 1 || max_compressed < 0) return OCC_E_SHAPE;
+  std::vector<StageTimes> st(n_stages);
+  for (int s = 0; s < n_stages; ++s) {
+    const occ_stage_t& x = stages[s];
+    for (double t : {x.bwd_done, x.comm, x.comm_compressed, x.compress})
+      if (!(t >= 0.0) || !std::isfinite(t)) return OCC_E_SHAPE;
+    st[s] = {x.bwd_done, x.comm, x.comm_compressed, x.compress};
+  }
+  const double end = sc_select(st.data(), n_stages, max_compressed, selected, n_selected);
+  if (t_end) *t_end = end;
   return OCC_OK;
 }
 

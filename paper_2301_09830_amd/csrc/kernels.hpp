@@ -22,7 +22,7 @@ __device__ __forceinline__ cfloat_p as_const(const float* p) { return (cfloat_p)
 __device__ __forceinline__ cdouble_p as_const(const double* p) { return (cdouble_p)(uintptr_t)p; }
 
 enum { DT_F32 = 0, DT_BF16 = 1 };
-enum : uint32_t { FLAG_NONFINITE = 1u, FLAG_RANK_DEFICIENT = 2u };
+enum : uint32_t { FLAG_NONFINITE = 1u, FLAG_RANK_DEFICIENT = 2u, FLAG_BAD_ROWS = 4u };
 
 // Index of this thread's wave in its block, as a wave-uniform (SGPR) value so
 // that addresses derived from it qualify for scalar loads.
@@ -57,15 +57,25 @@ __device__ __forceinline__ float m_elem(const Desc& d, int64_t off) {
   return __uint_as_float((uint32_t)h << 16);
 }
 
+// Row of M, err and M_hat that holds row `row` (< d.m) of the compressed
+// matrix: the same row, or with RM (row-sparse step) the row the validated
+// row list names.
+template <bool RM>
+__device__ __forceinline__ int64_t prow(const Desc& d, int row) {
+  if constexpr (RM) return (int64_t)d.rmap[row];
+  else return (int64_t)row;
+}
+
 // A[row, col..col+3] = M + err_prev for columns < c_hi (zero beyond, and for
 // rows >= m).  VEC requires 16-byte aligned fp32 rows (8-byte for bf16 M),
 // i.e. aligned bases, ld % 4 == 0 and col % 4 == 0.
-template <int DT, bool VEC>
+template <int DT, bool VEC, bool RM = false>
 __device__ __forceinline__ void load_a4(const Desc& d, int row, int col, int c_hi, float a[4]) {
   a[0] = a[1] = a[2] = a[3] = 0.f;
   if (row >= d.m || col >= c_hi) return;
-  const int64_t mo = (int64_t)row * d.ldm + col;
-  const int64_t eo = (int64_t)row * d.lde_in + col;
+  const int64_t pr = prow<RM>(d, row);
+  const int64_t mo = pr * d.ldm + col;
+  const int64_t eo = pr * d.lde_in + col;
   if (VEC && col + 4 <= c_hi) {
     if (DT == DT_F32) {
       const float4 v = *(const float4*)((const float*)d.M + mo);
@@ -315,6 +325,34 @@ __global__ void k_write_table(Desc* dst, TableChunk src, int n) {
 
 __global__ void k_zero_words(uint32_t* p, int n) {
   for (int i = threadIdx.x; i < n; i += blockDim.x) p[i] = 0u;
+}
+
+// Row list of the row-sparse step: rows[0 .. n) copied to dst, each index
+// clamped into [0, m_rows) so that no kernel can address outside M, err or
+// M_hat; an index out of range, or not larger than the one before it (the
+// list must be strictly increasing), raises FLAG_BAD_ROWS.  The streaming
+// kernels read the row map from the copy only.
+__global__ __launch_bounds__(kBlock) void k_rows_check(const int32_t* rows, int64_t n,
+                                                       int32_t m_rows, int32_t* dst,
+                                                       uint32_t* flags) {
+  bool bad = false;
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * kBlock) {
+    const int32_t v = rows[i];
+    bad = bad || v < 0 || v >= m_rows || (i > 0 && v <= rows[i - 1]);
+    dst[i] = v < 0 ? 0 : (v >= m_rows ? m_rows - 1 : v);
+  }
+  if (bad) atomicOr(flags, FLAG_BAD_ROWS);
+}
+
+// Row-sparse step with an empty row list: A is zero, so P_hat = 0 and
+// Q = A^T P_hat = 0 (the dense step on an all-zero matrix gives the same and
+// flags the rank deficiency).
+__global__ __launch_bounds__(kBlock) void k_rows_empty(float* Q, int64_t n, uint32_t* flags) {
+  for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * kBlock)
+    Q[i] = 0.f;
+  if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(flags, FLAG_RANK_DEFICIENT);
 }
 
 }  // namespace occ

@@ -114,24 +114,25 @@ struct RawA {
   float e[W];
 };
 
-template <int DT, int SA, int W>
+template <int DT, int SA, int W, bool RM = false>
 __device__ __forceinline__ RawA<DT, SA, W> rawa_load(const Desc& d, bool vec, int row, int c,
                                                     int c_hi) {
   RawA<DT, SA, W> x;
   if (vec && row < d.m && c + W <= c_hi) {
+    const int64_t pr = prow<RM>(d, row);
     if constexpr (SA == SA_SAVED) {
-      ld_f<W>(d.err_out + (int64_t)row * d.lde_out + c, x.e);
+      ld_f<W>(d.err_out + pr * d.lde_out + c, x.e);
       x.m[0] = 0u;
     } else {
       if constexpr (DT == DT_BF16) {
-        const uint16_t* mp = (const uint16_t*)d.M + (int64_t)row * d.ldm + c;
+        const uint16_t* mp = (const uint16_t*)d.M + pr * d.ldm + c;
         if constexpr (W == 1) x.m[0] = (uint32_t)(*mp) << 16;
         else ld_u<W / 2>((const uint32_t*)mp, x.m);
       } else {
-        ld_u<W>((const uint32_t*)((const float*)d.M + (int64_t)row * d.ldm + c), x.m);
+        ld_u<W>((const uint32_t*)((const float*)d.M + pr * d.ldm + c), x.m);
       }
       if (d.err_in) {
-        ld_f<W>(d.err_in + (int64_t)row * d.lde_in + c, x.e);
+        ld_f<W>(d.err_in + pr * d.lde_in + c, x.e);
       } else {
 #pragma unroll
         for (int j = 0; j < W; ++j) x.e[j] = -0.f;
@@ -142,11 +143,12 @@ __device__ __forceinline__ RawA<DT, SA, W> rawa_load(const Desc& d, bool vec, in
     for (int j = 0; j < W; ++j) {
       float v = 0.f;
       if (row < d.m && c + j < c_hi) {
+        const int64_t pr = prow<RM>(d, row);
         if constexpr (SA == SA_SAVED) {
-          v = d.err_out[(int64_t)row * d.lde_out + c + j];
+          v = d.err_out[pr * d.lde_out + c + j];
         } else {
-          v = m_elem<DT>(d, (int64_t)row * d.ldm + c + j);
-          if (d.err_in) v = v + d.err_in[(int64_t)row * d.lde_in + c + j];
+          v = m_elem<DT>(d, pr * d.ldm + c + j);
+          if (d.err_in) v = v + d.err_in[pr * d.lde_in + c + j];
         }
       }
       x.e[j] = v;
@@ -173,11 +175,11 @@ __device__ __forceinline__ float rawa_val(const RawA<DT, SA, W>& x, int j) {
 // Store W values of A over the error buffer (row < m).  Plain stores: the
 // stored A is read back by the next pass, and nontemporal stores measured
 // slower for the whole step.
-template <int W>
+template <int W, bool RM = false>
 __device__ __forceinline__ void a_store(const Desc& d, bool vec, int row, int c, int c_hi,
                                         const float* a) {
   if (row >= d.m) return;
-  float* p = d.err_out + (int64_t)row * d.lde_out + c;
+  float* p = d.err_out + prow<RM>(d, row) * d.lde_out + c;
   if (vec && c + W <= c_hi) {
     st_f<W>(p, a);
   } else {
@@ -352,7 +354,8 @@ __device__ __forceinline__ void lp_tile_store_a(const Desc& d, const uint8_t* sr
   }
 }
 
-template <int DT, int RP, int SA, bool X3, bool TILES>
+// RM (row-sparse step, register form only): rows through the row map.
+template <int DT, int RP, int SA, bool X3, bool TILES, bool RM = false>
 __device__ __forceinline__ void lp_body(const Desc& d, int b,
                                         std::conditional_t<X3, LPXSmem<RP>, LPSmem<RP>>& sm,
                                         uint8_t* tiles) {
@@ -467,6 +470,7 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b,
   // TILES: A tiles through LDS (the host picks this instance when rows are
   // 16-byte aligned, every K-step is whole and A has a source); else A goes
   // straight into registers.
+  static_assert(!(TILES && RM), "the row map runs on the register form");
   if constexpr (TILES) {
     constexpr int SB = LPTile<DT, SA>::BYTES;
     uint8_t* const wt = tiles + wave * 2 * SB;   // this wave's two stages
@@ -493,7 +497,7 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b,
     RawA<DT, SA, 16> ring[LP_DEPTH + 1];
 #pragma unroll
     for (int x = 0; x <= LP_DEPTH; ++x)
-      if (x < nk) ring[x] = rawa_load<DT, SA, 16>(d, vec, row, kcol_of(c_lo, ks0, x, nk) + 16 * g, c_hi);
+      if (x < nk) ring[x] = rawa_load<DT, SA, 16, RM>(d, vec, row, kcol_of(c_lo, ks0, x, nk) + 16 * g, c_hi);
     __syncthreads();
 
     int kc = kcol_of(c_lo, ks0, 0, nk);
@@ -502,12 +506,12 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b,
       float a[16];
 #pragma unroll
       for (int j = 0; j < 16; ++j) a[j] = rawa_val<DT, SA, 16>(ring[0], j);
-      if constexpr (SA == SA_MERR_SAVE) a_store<16>(d, vec, row, kc + 16 * g, c_hi, a);
+      if constexpr (SA == SA_MERR_SAVE) a_store<16, RM>(d, vec, row, kc + 16 * g, c_hi, a);
       mfma_step(a, it & 1);
 #pragma unroll
       for (int x = 0; x < LP_DEPTH; ++x) ring[x] = ring[x + 1];
       if (it + LP_DEPTH + 1 < nk)
-        ring[LP_DEPTH] = rawa_load<DT, SA, 16>(d, vec, row, kcol_of(c_lo, ks0, it + LP_DEPTH + 1, nk) + 16 * g, c_hi);
+        ring[LP_DEPTH] = rawa_load<DT, SA, 16, RM>(d, vec, row, kcol_of(c_lo, ks0, it + LP_DEPTH + 1, nk) + 16 * g, c_hi);
       if (it + 1 < nk) {
         // slot 0 now holds K-step it + 1
 #pragma unroll
@@ -532,11 +536,11 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b,
   }
 }
 
-template <int DT, int RP, int SA, bool X3, bool TILES>
+template <int DT, int RP, int SA, bool X3, bool TILES, bool RM = false>
 __global__ __launch_bounds__(kBlock) void k_lp(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) std::conditional_t<X3, LPXSmem<RP>, LPSmem<RP>> sm;
   __shared__ __attribute__((aligned(16))) uint8_t tiles[TILES ? 4 * 2 * LPTile<DT, SA>::BYTES : 16];
-#define B_(d, b) lp_body<DT, RP, SA, X3, TILES>(d, b, sm, tiles)
+#define B_(d, b) lp_body<DT, RP, SA, X3, TILES, RM>(d, b, sm, tiles)
   OCC_DISPATCH(K_PASS_P, B_)
 #undef B_
 }
@@ -1084,7 +1088,7 @@ struct LQSmem {
   float p[2][L_QG][RP + 4];
 };
 
-template <int DT, int RP, int SA>
+template <int DT, int RP, int SA, bool RM = false>
 __device__ __forceinline__ void lq_body(const Desc& d, int b, LQSmem<RP>& sm) {
   constexpr int NU = RP / 32, CPL = lq_cpl(RP), BC = lq_block_cols(RP);
   constexpr int PF = L_QG * RP / 4;   // float4s of one P_hat stage
@@ -1123,7 +1127,7 @@ __device__ __forceinline__ void lq_body(const Desc& d, int b, LQSmem<RP>& sm) {
 #pragma unroll
   for (int ks = 0; ks < 4; ++ks) {
     const int row = r_lo + 2 * ks + g;
-    cur[ks] = rawa_load<DT, SA, CPL>(d, vec, row < r_hi ? row : d.m, col, d.n);
+    cur[ks] = rawa_load<DT, SA, CPL, RM>(d, vec, row < r_hi ? row : d.m, col, d.n);
   }
   __syncthreads();
 
@@ -1141,7 +1145,7 @@ __device__ __forceinline__ void lq_body(const Desc& d, int b, LQSmem<RP>& sm) {
 #pragma unroll
       for (int ks = 0; ks < 4; ++ks) {
         const int row = rn + 2 * ks + g;
-        nxt[ks] = rawa_load<DT, SA, CPL>(d, vec, row < r_hi ? row : d.m, col, d.n);
+        nxt[ks] = rawa_load<DT, SA, CPL, RM>(d, vec, row < r_hi ? row : d.m, col, d.n);
       }
     }
 #pragma unroll
@@ -1310,8 +1314,9 @@ __device__ __forceinline__ void lq_tiles_body(const Desc& d, int b, uint8_t* til
   (void)col;
 }
 
-template <int DT, int RP, int SA, bool TILES>
+template <int DT, int RP, int SA, bool TILES, bool RM = false>
 __global__ __launch_bounds__(kBlock) void k_lq(OCC_KARGS) {
+  static_assert(!(TILES && RM), "the row map runs on the register form");
   if constexpr (TILES) {
     static_assert(DT == DT_F32 && SA == SA_SAVED, "tiles hold the stored fp32 A");
     __shared__ __attribute__((aligned(16))) uint8_t tiles[LQTile<RP>::AST * LQTile<RP>::STAGE];
@@ -1320,7 +1325,7 @@ __global__ __launch_bounds__(kBlock) void k_lq(OCC_KARGS) {
 #undef B_
   } else {
     __shared__ __attribute__((aligned(16))) LQSmem<RP> sm;
-#define B_(d, b) lq_body<DT, RP, SA>(d, b, sm)
+#define B_(d, b) lq_body<DT, RP, SA, RM>(d, b, sm)
     OCC_DISPATCH(K_PASS_Q, B_)
 #undef B_
   }
@@ -1404,8 +1409,9 @@ __device__ __forceinline__ void lqx_tile_read(const uint8_t* src, int li, int g,
   }
 }
 
-template <int DT, int RP, int SA, bool TILES>
+template <int DT, int RP, int SA, bool TILES, bool RM = false>
 __device__ __forceinline__ void lqx_body(const Desc& d, int b, LQXSmem<RP>& sm, uint8_t* tiles) {
+  static_assert(!(TILES && RM), "the row map runs on the register form");
   constexpr int NU = RP / 32, CPL = lq_cpl(RP), BC = lq_block_cols(RP);
   constexpr int NLD = 2 * NU;                         // P tile load instructions per group
   const bool vec = d.vec != 0;
@@ -1443,7 +1449,7 @@ __device__ __forceinline__ void lqx_body(const Desc& d, int b, LQXSmem<RP>& sm, 
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int row = r0 + 8 * g + e;
-      x[e] = rawa_load<DT, SA, CPL>(d, vec, row < r_hi ? row : d.m, col, d.n);
+      x[e] = rawa_load<DT, SA, CPL, RM>(d, vec, row < r_hi ? row : d.m, col, d.n);
     }
   };
 
@@ -1610,11 +1616,11 @@ __device__ __forceinline__ void lqx_body(const Desc& d, int b, LQXSmem<RP>& sm, 
   }
 }
 
-template <int DT, int RP, int SA, bool TILES>
+template <int DT, int RP, int SA, bool TILES, bool RM = false>
 __global__ __launch_bounds__(kBlock) void k_lqx(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) LQXSmem<RP> sm;
   __shared__ __attribute__((aligned(16))) uint8_t tiles[TILES ? 4 * LQXTile<RP>::AST * LQXTile<RP>::BYTES : 16];
-#define B_(d, b) lqx_body<DT, RP, SA, TILES>(d, b, sm, tiles)
+#define B_(d, b) lqx_body<DT, RP, SA, TILES, RM>(d, b, sm, tiles)
   OCC_DISPATCH(K_PASS_Q, B_)
 #undef B_
 }
@@ -1647,7 +1653,7 @@ __device__ __forceinline__ void lm_stage_direct(const Desc& d, int row0, float (
   }
 }
 
-template <int DT, int RP, int SA, int SRC, bool WM, bool WE, bool OUTBF = false>
+template <int DT, int RP, int SA, int SRC, bool WM, bool WE, bool OUTBF = false, bool RM = false>
 __device__ __forceinline__ void lm_body(const Desc& d, int b, LMSmem<RP>& sm) {
   constexpr int NCT = lm_tiles(RP), KP = RP / 2, BC = lm_block_cols(RP);
   constexpr int SF = RP * 8 / kBlock;   // float4s per thread per P_hat tile
@@ -1707,7 +1713,7 @@ __device__ __forceinline__ void lm_body(const Desc& d, int b, LMSmem<RP>& sm) {
       for (int c = 0; c < NCT; ++c)
 #pragma unroll
         for (int v = 0; v < 16; ++v)
-          av[c][v] = rawa_load<DT, SA, 1>(d, true, row0 + mf32_row(v, g), cw + 32 * c + li, d.n);
+          av[c][v] = rawa_load<DT, SA, 1, RM>(d, true, row0 + mf32_row(v, g), cw + 32 * c + li, d.n);
     }
     f16v acc[NCT];
 #pragma unroll
@@ -1727,10 +1733,11 @@ __device__ __forceinline__ void lm_body(const Desc& d, int b, LMSmem<RP>& sm) {
         const int row = row0 + mf32_row(v, g);
         if (row < r_hi && col < d.n) {
           const float mh = acc[c][v];
-          if (WM) store_mhat_nt<OUTBF>(d, (int64_t)row * d.ldh + col, mh);
+          const int64_t pr = prow<RM>(d, row);
+          if (WM) store_mhat_nt<OUTBF>(d, pr * d.ldh + col, mh);
           if (WE) {
             const float e = rawa_val<DT, SA, 1>(av[c][v], 0) - mh;
-            __builtin_nontemporal_store(e, d.err_out + (int64_t)row * d.lde_out + col);
+            __builtin_nontemporal_store(e, d.err_out + pr * d.lde_out + col);
           }
         }
       }
@@ -1750,10 +1757,10 @@ __device__ __forceinline__ void lm_body(const Desc& d, int b, LMSmem<RP>& sm) {
   }
 }
 
-template <int DT, int RP, int SA, int SRC, bool WM, bool WE, bool OUTBF = false>
+template <int DT, int RP, int SA, int SRC, bool WM, bool WE, bool OUTBF = false, bool RM = false>
 __global__ __launch_bounds__(kBlock) void k_ml(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) LMSmem<RP> sm;
-#define B_(d, b) lm_body<DT, RP, SA, SRC, WM, WE, OUTBF>(d, b, sm)
+#define B_(d, b) lm_body<DT, RP, SA, SRC, WM, WE, OUTBF, RM>(d, b, sm)
   OCC_DISPATCH(K_MHAT, B_)
 #undef B_
 }
@@ -1822,7 +1829,7 @@ __device__ __forceinline__ void lmx_stage(const f4v* pr, uint16_t (*dst)[32 * (R
   }
 }
 
-template <int RP, int SRC, bool WM, bool WE, bool OUTBF = false>
+template <int RP, int SRC, bool WM, bool WE, bool OUTBF = false, bool RM = false>
 __device__ __forceinline__ void lmx_body(const Desc& d, int b, LMXSmem<RP>& sm) {
   constexpr int NCT = lm_tiles(RP), KS = RP / 16, BC = lm_block_cols(RP);
   constexpr int SF = RP * 8 / kBlock;
@@ -1874,7 +1881,7 @@ __device__ __forceinline__ void lmx_body(const Desc& d, int b, LMXSmem<RP>& sm) 
       for (int c = 0; c < NCT; ++c)
 #pragma unroll
         for (int v = 0; v < 16; ++v)
-          av[c][v] = rawa_load<DT_F32, SA_SAVED, 1>(d, true, row0 + mf32_row(v, g), cw + 32 * c + li, d.n);
+          av[c][v] = rawa_load<DT_F32, SA_SAVED, 1, RM>(d, true, row0 + mf32_row(v, g), cw + 32 * c + li, d.n);
     }
     f16v acc[NCT];
 #pragma unroll
@@ -1900,10 +1907,11 @@ __device__ __forceinline__ void lmx_body(const Desc& d, int b, LMXSmem<RP>& sm) 
         const int row = row0 + mf32_row(v, g);
         if (row < r_hi && col < d.n) {
           const float mh = acc[c][v];
-          if (WM) store_mhat_nt<OUTBF>(d, (int64_t)row * d.ldh + col, mh);
+          const int64_t pr = prow<RM>(d, row);
+          if (WM) store_mhat_nt<OUTBF>(d, pr * d.ldh + col, mh);
           if (WE) {
             const float e = rawa_val<DT_F32, SA_SAVED, 1>(av[c][v], 0) - mh;
-            __builtin_nontemporal_store(e, d.err_out + (int64_t)row * d.lde_out + col);
+            __builtin_nontemporal_store(e, d.err_out + pr * d.lde_out + col);
           }
         }
       }
@@ -1913,10 +1921,10 @@ __device__ __forceinline__ void lmx_body(const Desc& d, int b, LMXSmem<RP>& sm) 
   }
 }
 
-template <int RP, int SRC, bool WM, bool WE, bool OUTBF = false>
+template <int RP, int SRC, bool WM, bool WE, bool OUTBF = false, bool RM = false>
 __global__ __launch_bounds__(kBlock) void k_mlx(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) LMXSmem<RP> sm;
-#define B_(d, b) lmx_body<RP, SRC, WM, WE, OUTBF>(d, b, sm)
+#define B_(d, b) lmx_body<RP, SRC, WM, WE, OUTBF, RM>(d, b, sm)
   OCC_DISPATCH(K_MHAT, B_)
 #undef B_
 }

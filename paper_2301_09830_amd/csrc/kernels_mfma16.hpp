@@ -85,11 +85,12 @@ __device__ __forceinline__ void ch8_neg_zero(Ch8<DT>& x) {
   }
 }
 
-template <int DT, bool VEC>
+template <int DT, bool VEC, bool RM = false>
 __device__ __forceinline__ Ch8<DT> ch8_load(const Desc& d, int row, int c, int c_hi) {
   Ch8<DT> x;
   if (VEC && row < d.m && c + 8 <= c_hi) {
-    const int64_t mo = (int64_t)row * d.ldm + c;
+    const int64_t pr = prow<RM>(d, row);
+    const int64_t mo = pr * d.ldm + c;
     if constexpr (DT == DT_BF16) {
       x.m = *(const uint4*)((const uint16_t*)d.M + mo);
     } else {
@@ -97,7 +98,7 @@ __device__ __forceinline__ Ch8<DT> ch8_load(const Desc& d, int row, int c, int c
       x.m1 = *(const float4*)((const float*)d.M + mo + 4);
     }
     if (d.err_in) {
-      const float* e = d.err_in + (int64_t)row * d.lde_in + c;
+      const float* e = d.err_in + pr * d.lde_in + c;
       x.e0 = *(const float4*)e;
       x.e1 = *(const float4*)(e + 4);
     } else {
@@ -106,8 +107,8 @@ __device__ __forceinline__ Ch8<DT> ch8_load(const Desc& d, int row, int c, int c
     }
   } else {
     float lo[4], hi[4];
-    load_a4<DT, false>(d, row, c, c_hi, lo);
-    load_a4<DT, false>(d, row, c + 4, c_hi, hi);
+    load_a4<DT, false, RM>(d, row, c, c_hi, lo);
+    load_a4<DT, false, RM>(d, row, c + 4, c_hi, hi);
     ch8_neg_zero<DT>(x);
     x.e0 = make_float4(lo[0], lo[1], lo[2], lo[3]);
     x.e1 = make_float4(hi[0], hi[1], hi[2], hi[3]);
@@ -235,7 +236,9 @@ __device__ __forceinline__ void pm_tile_issue(const Desc& d, const float* qs, in
                                        (lvoid_t*)(dst + 4 * PM_ESLOT + pm_mbytes<DT>() + 1024 * q), 16, 0, 0);
 }
 
-template <int DT, bool VEC, int RP>
+// RM (row-sparse step): rows through the row map, register loads only (the
+// tile path's wait counts assume its DMA instructions alone are in flight).
+template <int DT, bool VEC, int RP, bool RM = false>
 __device__ __forceinline__ void pm_body(const Desc& d, int b, PMSmem& sm) {
   const int wave = wave_id(), lane = threadIdx.x & 63;
   const int li = lane & 15, g = lane >> 4;
@@ -272,7 +275,7 @@ __device__ __forceinline__ void pm_body(const Desc& d, int b, PMSmem& sm) {
   // 16-byte aligned Q: tiles through LDS (the condition is the same for the
   // whole launch); otherwise loads straight into registers.
   bool dma = false;
-  if constexpr (VEC) {
+  if constexpr (VEC && !RM) {
     dma = d.err_in != nullptr && (d.n & 31) == 0 && ((uintptr_t)qs & 15) == 0;
     if (dma) {
       // This wave's K-steps ks = wave + PM_WAVES * it; step it lives in stage
@@ -364,7 +367,7 @@ __device__ __forceinline__ void pm_body(const Desc& d, int b, PMSmem& sm) {
       const int c = kcol(ks);
       cq = q8_load<RP>(qs, d.n, c, li);
 #pragma unroll
-      for (int r = 0; r < PM_RB; ++r) cur[r] = ch8_load<DT, VEC>(d, row0 + 16 * r + li, c, d.n);
+      for (int r = 0; r < PM_RB; ++r) cur[r] = ch8_load<DT, VEC, RM>(d, row0 + 16 * r + li, c, d.n);
     }
     for (; ks < nk; ks += PM_WAVES) {
       const bool more = ks + PM_WAVES < nk;
@@ -372,7 +375,7 @@ __device__ __forceinline__ void pm_body(const Desc& d, int b, PMSmem& sm) {
       if (more) {
         nq = q8_load<RP>(qs, d.n, cn, li);
 #pragma unroll
-        for (int r = 0; r < PM_RB; ++r) nxt[r] = ch8_load<DT, VEC>(d, row0 + 16 * r + li, cn, d.n);
+        for (int r = 0; r < PM_RB; ++r) nxt[r] = ch8_load<DT, VEC, RM>(d, row0 + 16 * r + li, cn, d.n);
       }
       mfma_step(cur, cq);
       if (more) {
@@ -403,10 +406,10 @@ __device__ __forceinline__ void pm_body(const Desc& d, int b, PMSmem& sm) {
   gram_rows_store<RP, PM_THREADS>(sm.e.rows, nr, d.gpart + (int64_t)b * (RP * (RP + 1) / 2));
 }
 
-template <int DT, bool VEC, int RP>
+template <int DT, bool VEC, int RP, bool RM = false>
 __global__ __launch_bounds__(PM_THREADS) void k_pm(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) PMSmem sm;
-#define B_(d, b) pm_body<DT, VEC, RP>(d, b, sm)
+#define B_(d, b) pm_body<DT, VEC, RP, RM>(d, b, sm)
   OCC_DISPATCH(K_PASS_P, B_)
 #undef B_
 }
@@ -424,7 +427,7 @@ struct QMSmem {
   } u;
 };
 
-template <int DT, bool VEC, int RP>
+template <int DT, bool VEC, int RP, bool RM = false>
 __device__ __forceinline__ void qm_body(const Desc& d, int b, QMSmem& sm) {
   const int wave = wave_id(), lane = threadIdx.x & 63;
   const int li = lane & 15, g = lane >> 4;
@@ -449,7 +452,7 @@ __device__ __forceinline__ void qm_body(const Desc& d, int b, QMSmem& sm) {
   {
     const int row = w_lo + g;
     const bool ok = row < w_hi;
-    cur = ch8_load<DT, VEC>(d, ok ? row : d.m, col, d.n);
+    cur = ch8_load<DT, VEC, RM>(d, ok ? row : d.m, col, d.n);
     cp = (ok && li < RP) ? ps[(int64_t)row * RP + li] : 0.f;
   }
   for (int ks = 0; ks < nk; ++ks) {
@@ -457,7 +460,7 @@ __device__ __forceinline__ void qm_body(const Desc& d, int b, QMSmem& sm) {
     if (more) {
       const int row = w_lo + 4 * (ks + 1) + g;
       const bool ok = row < w_hi;
-      nxt = ch8_load<DT, VEC>(d, ok ? row : d.m, col, d.n);
+      nxt = ch8_load<DT, VEC, RM>(d, ok ? row : d.m, col, d.n);
       np = (ok && li < RP) ? ps[(int64_t)row * RP + li] : 0.f;
     }
     float a[8];
@@ -488,10 +491,10 @@ __device__ __forceinline__ void qm_body(const Desc& d, int b, QMSmem& sm) {
   }
 }
 
-template <int DT, bool VEC, int RP>
+template <int DT, bool VEC, int RP, bool RM = false>
 __global__ __launch_bounds__(QM_THREADS) void k_qm(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) QMSmem sm;
-#define B_(d, b) qm_body<DT, VEC, RP>(d, b, sm)
+#define B_(d, b) qm_body<DT, VEC, RP, RM>(d, b, sm)
   OCC_DISPATCH(K_PASS_Q, B_)
 #undef B_
 }
@@ -561,7 +564,8 @@ __device__ __forceinline__ void factor_load(const float* base, int r, int row, b
 
 // OUTBF (stand-alone decompression only): M_hat is stored as bf16, each
 // element rounded to nearest even from the fp32 result.
-template <int DT, bool VEC, int RP, int SRC, bool WRITE_MHAT, bool WRITE_ERR, bool OUTBF = false>
+template <int DT, bool VEC, int RP, int SRC, bool WRITE_MHAT, bool WRITE_ERR, bool OUTBF = false,
+          bool RM = false>
 __device__ __forceinline__ void mh16_body(const Desc& d, int b, MXSmem& sm) {
   constexpr int S = RP / 4;        // MFMA K-steps (rank indices per lane group)
   constexpr int NTILE = F_MHCOLS / 16;
@@ -591,7 +595,7 @@ __device__ __forceinline__ void mh16_body(const Desc& d, int b, MXSmem& sm) {
 #pragma unroll
       for (int k = 0; k < MX_NCH; ++k) {
         const int row = r0 + rl + MX_RPI * k;
-        chunk_issue<DT, VEC>(d, row < r_hi ? row : d.m, col, d.n, x[k]);
+        chunk_issue<DT, VEC, RM>(d, row < r_hi ? row : d.m, col, d.n, x[k]);
       }
     }
     // B operand: P_hat[r0 + li][S g + s]
@@ -614,6 +618,7 @@ __device__ __forceinline__ void mh16_body(const Desc& d, int b, MXSmem& sm) {
       const int row = r0 + rr;
       const float4 mh4 = *(const float4*)(tile + rr * MX_LDW + cl);
       if (row >= r_hi) continue;
+      const int64_t pr = prow<RM>(d, row);
       const float mh[4] = {mh4.x, mh4.y, mh4.z, mh4.w};
       float e[4] = {0.f, 0.f, 0.f, 0.f};
       if (WRITE_ERR) {
@@ -629,19 +634,19 @@ __device__ __forceinline__ void mh16_body(const Desc& d, int b, MXSmem& sm) {
         typedef uint32_t nu2 __attribute__((ext_vector_type(2)));
         if (WRITE_MHAT && OUTBF)
           __builtin_nontemporal_store(nu2{bf16_pack2(mh[0], mh[1]), bf16_pack2(mh[2], mh[3])},
-                                      (nu2*)((uint16_t*)d.Mhat + (int64_t)row * d.ldh + col));
+                                      (nu2*)((uint16_t*)d.Mhat + pr * d.ldh + col));
         else if (WRITE_MHAT)
           __builtin_nontemporal_store(nt4{mh[0], mh[1], mh[2], mh[3]},
-                                      (nt4*)(d.Mhat + (int64_t)row * d.ldh + col));
+                                      (nt4*)(d.Mhat + pr * d.ldh + col));
         if (WRITE_ERR)
           __builtin_nontemporal_store(nt4{e[0], e[1], e[2], e[3]},
-                                      (nt4*)(d.err_out + (int64_t)row * d.lde_out + col));
+                                      (nt4*)(d.err_out + pr * d.lde_out + col));
       } else {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           if (col + j < d.n) {
-            if (WRITE_MHAT) store_mhat1<OUTBF>(d, (int64_t)row * d.ldh + col + j, mh[j]);
-            if (WRITE_ERR) d.err_out[(int64_t)row * d.lde_out + col + j] = e[j];
+            if (WRITE_MHAT) store_mhat1<OUTBF>(d, pr * d.ldh + col + j, mh[j]);
+            if (WRITE_ERR) d.err_out[pr * d.lde_out + col + j] = e[j];
           }
         }
       }
@@ -650,10 +655,11 @@ __device__ __forceinline__ void mh16_body(const Desc& d, int b, MXSmem& sm) {
   }
 }
 
-template <int DT, bool VEC, int RP, int SRC, bool WRITE_MHAT, bool WRITE_ERR, bool OUTBF = false>
+template <int DT, bool VEC, int RP, int SRC, bool WRITE_MHAT, bool WRITE_ERR, bool OUTBF = false,
+          bool RM = false>
 __global__ __launch_bounds__(kBlock) void k_mh16(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) MXSmem sm;
-#define B_(d, b) mh16_body<DT, VEC, RP, SRC, WRITE_MHAT, WRITE_ERR, OUTBF>(d, b, sm)
+#define B_(d, b) mh16_body<DT, VEC, RP, SRC, WRITE_MHAT, WRITE_ERR, OUTBF, RM>(d, b, sm)
   OCC_DISPATCH(K_MHAT, B_)
 #undef B_
 }

@@ -45,17 +45,18 @@ __device__ __forceinline__ typename MVec<DT>::T neg_zero_m() {
 
 // Fast path: whole chunk in bounds and VEC layout; otherwise the exact
 // element-wise A is stored in `e` and `m` holds -0 (x + -0 == x for all x).
-template <int DT, bool VEC>
+template <int DT, bool VEC, bool RM = false>
 __device__ __forceinline__ void chunk_issue(const Desc& d, int row, int col, int c_hi,
                                             AChunk<DT>& x) {
   if (VEC && row < d.m && col + 4 <= c_hi) {
-    const int64_t mo = (int64_t)row * d.ldm + col;
+    const int64_t pr = prow<RM>(d, row);
+    const int64_t mo = pr * d.ldm + col;
     x.m = *(const typename MVec<DT>::T*)((const char*)d.M + mo * (DT == DT_F32 ? 4 : 2));
-    x.e = d.err_in ? *(const float4*)(d.err_in + (int64_t)row * d.lde_in + col)
+    x.e = d.err_in ? *(const float4*)(d.err_in + pr * d.lde_in + col)
                    : make_float4(-0.f, -0.f, -0.f, -0.f);
   } else {
     float a[4];
-    load_a4<DT, false>(d, row, col, c_hi, a);
+    load_a4<DT, false, RM>(d, row, col, c_hi, a);
     x.m = neg_zero_m<DT>();
     x.e = make_float4(a[0], a[1], a[2], a[3]);
   }

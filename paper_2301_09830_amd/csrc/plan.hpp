@@ -54,6 +54,8 @@ struct Desc {
   float* phat_t;         // large-rank path: P_hat transposed, rp x m_pad
   uint16_t* qbf;         // large-rank path, bf16 M: Q as bf16 hi/lo parts, [2][rp][n_pad],
                          // rank k in row (k % (rp/32)) * 32 + k / (rp/32)
+  const int32_t* rmap;   // row-sparse step: row i of the compressed matrix is row rmap[i]
+                         // of M, err and M_hat (validated copy in the workspace); else null
   // shapes
   int32_t m, n, r;
   int32_t ldm, lde_in, lde_out, ldh;
@@ -94,7 +96,6 @@ constexpr int F_MHGROUP = 64;     // reconstruction: rows per block step (4 wave
 constexpr int F_MHBLOCKS = 1024;  // reconstruction: target number of blocks
 constexpr int F_QBLOCKS = 512;    // right product: target number of blocks
 constexpr int F_ORTHROWS = 128;   // Cholesky/P_hat kernel: rows of P_hat per block
-
 // Large-rank path (padded rank 32, 64, 128): tile constants shared with
 // kernels_large.hpp.
 constexpr int L_PROWS = 128;      // left product: rows per block (4 waves x 32)

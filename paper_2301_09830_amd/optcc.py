@@ -23,7 +23,7 @@ HEADER = os.path.join(os.path.dirname(PKG), "include", "optcc.h")
 
 OCC_OK = 0
 OCC_F32, OCC_BF16 = 0, 1
-OCC_F_NONFINITE, OCC_F_RANK_DEFICIENT = 1, 2
+OCC_F_NONFINITE, OCC_F_RANK_DEFICIENT, OCC_F_BAD_ROWS = 1, 2, 4
 OCC_NO_MHAT = 1
 OCC_DEC_SPLIT_BF16, OCC_DEC_OUT_BF16 = 1, 2
 OCC_MAX_RANK = 128
@@ -59,6 +59,15 @@ class occ_mat_t(ctypes.Structure):
         ("Q", ctypes.c_void_p),
         ("M_hat", ctypes.c_void_p),
         ("ldh", ctypes.c_int64),
+    ]
+
+
+class occ_stage_t(ctypes.Structure):
+    _fields_ = [
+        ("bwd_done", ctypes.c_double),
+        ("comm", ctypes.c_double),
+        ("comm_compressed", ctypes.c_double),
+        ("compress", ctypes.c_double),
     ]
 
 
@@ -100,8 +109,20 @@ _SIGS = {
     "occ_step_batched": (ctypes.c_int, [ctypes.POINTER(occ_mat_t), ctypes.c_int, ctypes.c_int,
                                         ctypes.c_int, ctypes.c_uint, ctypes.c_void_p,
                                         ctypes.c_size_t, ctypes.c_void_p]),
+    "occ_step_rows": (ctypes.c_int, [ctypes.POINTER(occ_mat_t), ctypes.c_void_p, ctypes.c_int64,
+                                     ctypes.c_int, ctypes.c_int, ctypes.c_uint, ctypes.c_void_p,
+                                     ctypes.c_size_t, ctypes.c_void_p]),
+    "occ_step_rows_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int64, ctypes.c_int64,
+                                                        ctypes.c_int, ctypes.c_int, ctypes.c_int]),
     "occ_get_flags": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_uint32),
                                      ctypes.c_int, ctypes.c_void_p]),
+    "occ_pipeline_1f1b": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, ctypes.c_double,
+                                         ctypes.c_double, ctypes.c_double,
+                                         ctypes.POINTER(ctypes.c_double),
+                                         ctypes.POINTER(ctypes.c_double)]),
+    "occ_sc_select": (ctypes.c_int, [ctypes.POINTER(occ_stage_t), ctypes.c_int, ctypes.c_int,
+                                     ctypes.POINTER(ctypes.c_uint8), ctypes.POINTER(ctypes.c_int),
+                                     ctypes.POINTER(ctypes.c_double)]),
     "occ_profile_begin": (ctypes.c_int, []),
     "occ_profile_end": (ctypes.c_int, [ctypes.POINTER(occ_kernel_time_t), ctypes.c_int,
                                        ctypes.POINTER(ctypes.c_int)]),
@@ -281,6 +302,52 @@ def occ_step_batched(items, rank: int, iters: int, write_mhat: bool = True, ws=N
     return ws
 
 
+def occ_step_rows_workspace_bytes(n_rows: int, cols: int, rank: int, iters: int,
+                                  m_dtype: int = OCC_F32) -> int:
+    return int(lib().occ_step_rows_workspace_bytes(n_rows, cols, m_dtype, rank, iters))
+
+
+def occ_step_rows(M, err, Q, rows, rank: int, iters: int, P=None, M_hat=None,
+                  write_mhat: bool = True, ws=None, stream=None):
+    """Row-sparse step: compress the listed rows of M + err (rows: int32 CUDA
+    tensor, strictly increasing); err and Q updated in place, only the listed
+    rows of err and M_hat are written.  Returns (P, M_hat) with P compact
+    (len(rows) x rank).  A newly allocated M_hat is zero-filled, so that its
+    unlisted rows hold the dense step's zeros."""
+    torch = _torch()
+    m, n = M.shape
+    if rows.dtype != torch.int32 or rows.dim() != 1 or not rows.is_contiguous():
+        raise TypeError("rows must be a contiguous 1-D int32 tensor")
+    n_rows = int(rows.numel())
+    if P is None:
+        P = torch.empty((n_rows, rank), dtype=torch.float32, device=M.device)
+    if write_mhat and M_hat is None:
+        M_hat = torch.zeros((m, n), dtype=torch.float32, device=M.device)
+    _f32(err, "err"), _f32(P, "P"), _f32(Q, "Q"), _f32(M_hat, "M_hat")
+    if P.shape != (n_rows, rank) or Q.shape != (n, rank) or not (P.is_contiguous() and
+                                                                 Q.is_contiguous()):
+        raise ValueError("P must be len(rows) x rank and Q cols x rank, both contiguous")
+    a = occ_mat_t()
+    a.M = _ptr(M)
+    a.m_dtype = _mdtype(M)
+    a.rows, a.cols = m, n
+    a.ldm = _ld(M, "M")
+    a.err = _ptr(err)
+    a.lde = _ld(err, "err")
+    a.P = _ptr(P) if n_rows else None
+    a.Q = _ptr(Q)
+    a.M_hat = _ptr(M_hat) if write_mhat else None
+    a.ldh = _ld(M_hat, "M_hat") if write_mhat else 0
+    if ws is None:
+        ws = alloc_workspace(occ_step_rows_workspace_bytes(n_rows, n, rank, iters, a.m_dtype),
+                             M.device, stream)
+    flags = 0 if write_mhat else OCC_NO_MHAT
+    _check("occ_step_rows", lib().occ_step_rows(ctypes.byref(a), _ptr(rows) if n_rows else None,
+                                                n_rows, rank, iters, flags, _ptr(ws), ws.numel(),
+                                                _stream(stream)))
+    return P, (M_hat if write_mhat else None)
+
+
 def occ_compress(M, err_prev, Q, rank: int, iters: int, P=None, ws=None, stream=None):
     """A = M + err_prev (err_prev may be None); Q updated in place; returns P_hat."""
     torch = _torch()
@@ -345,6 +412,28 @@ def occ_err_update(M, err_prev, M_hat, err_new=None, stream=None):
                                                   _ld(M_hat, "M_hat"), _ptr(err_new),
                                                   _stream(stream)))
     return err_new
+
+
+def occ_pipeline_1f1b(n_stages: int, n_micro: int, t_fwd: float, t_bwd: float,
+                      t_p2p: float = 0.0):
+    """(bwd_done per stage, end of the schedule) under one-forward-one-backward."""
+    out = (ctypes.c_double * n_stages)()
+    end = ctypes.c_double(0.0)
+    _check("occ_pipeline_1f1b", lib().occ_pipeline_1f1b(n_stages, n_micro, t_fwd, t_bwd, t_p2p,
+                                                        out, ctypes.byref(end)))
+    return list(out), end.value
+
+
+def occ_sc_select(stages, max_compressed: int):
+    """stages: sequence of (bwd_done, comm, comm_compressed, compress).
+    Returns (selected flags per stage, end of the last exchange)."""
+    arr = (occ_stage_t * len(stages))(*[occ_stage_t(*map(float, t)) for t in stages])
+    sel = (ctypes.c_uint8 * len(stages))()
+    n = ctypes.c_int(0)
+    end = ctypes.c_double(0.0)
+    _check("occ_sc_select", lib().occ_sc_select(arr, len(stages), max_compressed, sel,
+                                                ctypes.byref(n), ctypes.byref(end)))
+    return [int(x) for x in sel], end.value
 
 
 def occ_get_flags(ws, clear: bool = False, stream=None) -> int:

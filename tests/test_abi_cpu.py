@@ -131,3 +131,32 @@ def test_workspace_size_is_deterministic_and_grows(L):
     # config sizes stay modest relative to the 288 GB HBM
     w5 = optcc.occ_workspace_bytes([(16384, 8192)] * 4, 128, 2)
     assert w5 < 2 << 30
+
+
+def test_rows_step_validates_on_the_host(L):
+    a = _mat(rows=64, cols=32)
+    ws, nb = 1 << 32, 1 << 30
+    rows = 1 << 36
+    # fewer listed rows than the rank, more rows than the matrix, negative count
+    assert L.occ_step_rows(ctypes.byref(a), rows, 3, 4, 1, 0, ws, nb, None) == 3
+    assert L.occ_step_rows(ctypes.byref(a), rows, 65, 4, 1, 0, ws, nb, None) == 2
+    assert L.occ_step_rows(ctypes.byref(a), rows, -1, 4, 1, 0, ws, nb, None) == 2
+    # missing row list, unaligned row list, list overlapping err
+    assert L.occ_step_rows(ctypes.byref(a), None, 10, 4, 1, 0, ws, nb, None) == 1
+    assert L.occ_step_rows(ctypes.byref(a), rows + 2, 10, 4, 1, 0, ws, nb, None) == 6
+    assert L.occ_step_rows(ctypes.byref(a), a.err + 64, 10, 4, 1, 0, ws, nb, None) == 7
+    # workspace too small for the listed rows, unknown flag
+    need = L.occ_step_rows_workspace_bytes(10, 32, 0, 4, 1)
+    assert need > 0
+    assert L.occ_step_rows(ctypes.byref(a), rows, 10, 4, 1, 0, ws, need - 256, None) == 8
+    assert L.occ_step_rows(ctypes.byref(a), rows, 10, 4, 1, 2, ws, nb, None) == 10
+    assert L.occ_step_rows(None, rows, 10, 4, 1, 0, ws, nb, None) == 1
+
+
+def test_rows_workspace_grows_with_the_list(L):
+    a = L.occ_step_rows_workspace_bytes(100, 3072, 0, 64, 1)
+    b = L.occ_step_rows_workspace_bytes(2500, 3072, 0, 64, 1)
+    dense = optcc.occ_workspace_bytes([(51200, 3072)], 64, 1)
+    assert 0 < a < b < dense
+    assert L.occ_step_rows_workspace_bytes(0, 3072, 0, 64, 1) == 256
+    assert L.occ_step_rows_workspace_bytes(10, 3072, 0, 64, 1) == 0     # rows < rank
