@@ -212,6 +212,21 @@ occ_status_t occ_step_rows(const occ_mat_t* mat, const int32_t* rows, int64_t n_
 size_t occ_step_rows_workspace_bytes(int64_t n_rows, int64_t cols, int m_dtype, int rank,
                                      int iters);
 
+/* occ_step_batched without a workspace argument and without any device
+ * allocation, for callers that cannot allocate: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  The
+ * workspace is a static device array of OCC_NOALLOC_MAX_BYTES inside the
+ * library (one per GPU, held until the process ends); a call whose
+ * occ_workspace_bytes exceeds it returns OCC_E_WORKSPACE before anything is
+ * enqueued.  Every call on one GPU shares that GPU's array: calls that
+ * overlap in time on one GPU (other streams, other threads) race, so callers
+ * order them.  Numeric flags are OR-ed into *flags_out (a DEVICE word the
+ * caller owns and clears), or dropped when flags_out is NULL.  Results are
+ * bitwise those of occ_step_batched on the same arguments. */
+#define OCC_NOALLOC_MAX_BYTES ((size_t)64 << 20)
+occ_status_t occ_step_batched_noalloc(const occ_mat_t* mats, int count, int rank, int iters,
+                                      unsigned flags, uint32_t* flags_out, occ_stream_t stream);
+
 /* Selective stage compression (Sec. 7), host-side model.  With pipeline
  * parallelism the later stages finish their backward passes first and start
  * their data-parallel gradient exchange early; the exchange of the earliest

@@ -12,5 +12,5 @@ from .optcc import (OCC_BF16, OCC_DEC_OUT_BF16, OCC_DEC_SPLIT_BF16, OCC_F32,  # 
                     occ_compress_workspace_bytes, occ_decompress, occ_decompress_ex,
                     occ_err_update, occ_get_flags, occ_pipeline_1f1b, occ_profile_begin,
                     occ_profile_end, occ_sc_select, occ_status_str, occ_step, occ_step_batched,
-                    occ_step_rows, occ_step_rows_workspace_bytes,
+                    occ_step_batched_noalloc, occ_step_rows, occ_step_rows_workspace_bytes,
                     occ_workspace_bytes, occ_workspace_init)

@@ -24,6 +24,12 @@
 
 using namespace occ;
 
+// Workspace of occ_step_batched_noalloc: one array per GPU, resident for the
+// life of the process.  Host code never uses this name as an address (it is
+// a host-side stand-in); it takes each device's address from
+// hipGetSymbolAddress once per device (noalloc_scratch below).
+static __device__ __align__(256) uint8_t scratch[OCC_NOALLOC_MAX_BYTES];
+
 namespace {
 
 // ----------------------------------------------------------------------------
@@ -590,6 +596,32 @@ occ_status_t plan_rows(const occ_mat_t* mat, int64_t n_rows, int rank, int iters
 
 }  // namespace
 
+namespace {
+
+// Device address of `scratch` on the current device, looked up once per device
+// with that device current; nullptr if the runtime cannot provide it.
+void* noalloc_scratch() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  static std::mutex mu;
+  static std::map<int, void*> addr;
+  std::lock_guard<std::mutex> lock(mu);
+  const auto it = addr.find(dev);
+  if (it != addr.end()) return it->second;
+  void* p = nullptr;
+  if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  addr[dev] = p;
+  return p;
+}
+
+}  // namespace
+
 // ============================================================================
 // C ABI
 // ============================================================================
@@ -644,6 +676,21 @@ occ_status_t occ_step_batched(const occ_mat_t* mats, int count, int rank, int it
   Batch b;
   OCC_TRY(plan_batch(mats, count, rank, iters, flags, ws, ws_bytes, false, b));
   return run_batch(b, ws, (uint32_t*)ws, true, !(flags & OCC_NO_MHAT), (hipStream_t)stream);
+}
+
+occ_status_t occ_step_batched_noalloc(const occ_mat_t* mats, int count, int rank, int iters,
+                                      unsigned flags, uint32_t* flags_out, occ_stream_t stream) {
+  Batch b;
+  OCC_TRY(plan_batch(mats, count, rank, iters, flags, nullptr, 0, true, b));
+  if (b.ws_needed > OCC_NOALLOC_MAX_BYTES) return OCC_E_WORKSPACE;
+  if (flags_out && !aligned(flags_out, 4)) return OCC_E_ALIGN;
+  void* ws = noalloc_scratch();
+  if (!ws) return OCC_E_HIP;
+  OCC_TRY(plan_batch(mats, count, rank, iters, flags, ws, OCC_NOALLOC_MAX_BYTES, false, b));
+  // the scratch header is the flag word when the caller passes none; nothing
+  // else in it needs to start at zero (every region is written before it is read)
+  uint32_t* fl = flags_out ? flags_out : (uint32_t*)ws;
+  return run_batch(b, ws, fl, true, !(flags & OCC_NO_MHAT), (hipStream_t)stream);
 }
 
 occ_status_t occ_step(const occ_mat_t* mat, int rank, int iters, unsigned flags, void* ws,

@@ -27,6 +27,7 @@ OCC_F_NONFINITE, OCC_F_RANK_DEFICIENT, OCC_F_BAD_ROWS = 1, 2, 4
 OCC_NO_MHAT = 1
 OCC_DEC_SPLIT_BF16, OCC_DEC_OUT_BF16 = 1, 2
 OCC_MAX_RANK = 128
+OCC_NOALLOC_MAX_BYTES = 64 << 20
 OCC_MAX_ITERS = 64
 
 STATUS_NAMES = {
@@ -114,6 +115,9 @@ _SIGS = {
                                      ctypes.c_size_t, ctypes.c_void_p]),
     "occ_step_rows_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int64, ctypes.c_int64,
                                                         ctypes.c_int, ctypes.c_int, ctypes.c_int]),
+    "occ_step_batched_noalloc": (ctypes.c_int, [ctypes.POINTER(occ_mat_t), ctypes.c_int,
+                                                ctypes.c_int, ctypes.c_int, ctypes.c_uint,
+                                                ctypes.c_void_p, ctypes.c_void_p]),
     "occ_get_flags": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_uint32),
                                      ctypes.c_int, ctypes.c_void_p]),
     "occ_pipeline_1f1b": (ctypes.c_int, [ctypes.c_int, ctypes.c_int, ctypes.c_double,
@@ -300,6 +304,23 @@ def occ_step_batched(items, rank: int, iters: int, write_mhat: bool = True, ws=N
     _check("occ_step_batched", lib().occ_step_batched(arr, len(items), rank, iters, flags,
                                                       _ptr(ws), ws.numel(), _stream(stream)))
     return ws
+
+
+def occ_step_batched_noalloc(items, rank: int, iters: int, write_mhat: bool = True,
+                             flags_out=None, stream=None) -> None:
+    """occ_step_batched on the library's static per-GPU workspace (no device
+    allocation by the library or by this binding).  items as for
+    occ_step_batched; flags_out: optional int32 CUDA tensor of one element
+    that receives the numeric flags (OR-ed in)."""
+    arr = (occ_mat_t * len(items))()
+    for a, (M, err, Q, P, M_hat) in zip(arr, items):
+        ctypes.memmove(ctypes.byref(a), ctypes.byref(make_mat(M, err, P, Q,
+                                                              M_hat if write_mhat else None)),
+                       ctypes.sizeof(occ_mat_t))
+    flags = 0 if write_mhat else OCC_NO_MHAT
+    _check("occ_step_batched_noalloc",
+           lib().occ_step_batched_noalloc(arr, len(items), rank, iters, flags, _ptr(flags_out),
+                                          _stream(stream)))
 
 
 def occ_step_rows_workspace_bytes(n_rows: int, cols: int, rank: int, iters: int,

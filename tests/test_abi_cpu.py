@@ -160,3 +160,16 @@ def test_rows_workspace_grows_with_the_list(L):
     assert 0 < a < b < dense
     assert L.occ_step_rows_workspace_bytes(0, 3072, 0, 64, 1) == 256
     assert L.occ_step_rows_workspace_bytes(10, 3072, 0, 64, 1) == 0     # rows < rank
+
+
+def test_noalloc_rejects_calls_beyond_its_static_workspace(L):
+    """The 36 stage-weight matrices need about 386 MiB of workspace, beyond the
+    64 MiB static array: rejected on the host before any device call."""
+    from workloads import WORKLOADS
+    shapes = WORKLOADS[3].shapes
+    arr = (optcc.occ_mat_t * len(shapes))()
+    for j, (m, n) in enumerate(shapes):
+        arr[j] = _mat(rows=m, cols=n, base=(j + 1) << 34)
+    assert optcc.occ_workspace_bytes(list(shapes), 32, 2) > optcc.OCC_NOALLOC_MAX_BYTES
+    assert L.occ_step_batched_noalloc(arr, len(shapes), 32, 2, 0, None, None) == 8
+    assert L.occ_step_batched_noalloc(arr, len(shapes), 32, 2, 4, None, None) == 10
