@@ -292,6 +292,7 @@ occ_status_t plan_batch(const occ_mat_t* mats, int count, int rank, int iters, u
     d.sp = t.sp;
     d.p_cols = t.p_cols;
     d.ng = t.ng;
+    d.grows = t.grows;
     d.sq = t.sq;
     d.q_rows = t.q_rows;
     d.m_pad = t.m_pad;
@@ -433,10 +434,12 @@ occ_status_t run_batch_t(const Batch& b, void* ws, uint32_t* flags, bool finish,
         // bf16 M: left products on bf16 matrix cores with split operands
         constexpr bool X3 = DT == DT_BF16;
         // left products with their A tiles through LDS when every row is
-        // 16-byte aligned, every 32-column K-step whole and A has a source
-        // (never with a row map: TL instances are the register forms then)
-        constexpr bool TL = !RM;
-        bool whole = VEC && TL;
+        // 16-byte aligned, every 32-column K-step whole and A has a source.
+        // With a row map only the first left product (M and err_prev rows)
+        // and the reconstruction (err and M_hat rows) use it: the stored A is
+        // compact, so every pass in between is the dense kernel.
+        constexpr bool TL = true;
+        bool whole = VEC;
         for (const Desc& dd : b.descs) whole = whole && dd.n % 32 == 0;
         const bool tiles_merr = whole && b.descs[0].err_in != nullptr;
         L("qpad", k_qpadl<RP>, b.blocks[K_QPAD]);
@@ -453,9 +456,9 @@ occ_status_t run_batch_t(const Batch& b, void* ws, uint32_t* flags, bool finish,
               L("pass_p_first", k_lp<DT, RP, SA_MERR_SAVE, X3, false, RM>, b.blocks[K_PASS_P]);
           } else {
             if (whole)
-              L("pass_p_a", k_lp<DT_F32, RP, SA_SAVED, X3, TL, RM>, b.blocks[K_PASS_P]);
+              L("pass_p_a", k_lp<DT_F32, RP, SA_SAVED, X3, TL>, b.blocks[K_PASS_P]);
             else
-              L("pass_p_a", k_lp<DT_F32, RP, SA_SAVED, X3, false, RM>, b.blocks[K_PASS_P]);
+              L("pass_p_a", k_lp<DT_F32, RP, SA_SAVED, X3, false>, b.blocks[K_PASS_P]);
           }
           L("gram", k_lg<RP, 0>, b.blocks[K_PGRAM]);
           L("gram_sum", k_gsum<RP, 0>, b.blocks[K_GSUM]);
@@ -468,16 +471,16 @@ occ_status_t run_batch_t(const Batch& b, void* ws, uint32_t* flags, bool finish,
           if constexpr (X3) {
             // the stored A through LDS tiles under the same conditions
             if (saved && whole)
-              L("pass_q_a", k_lqx<DT_F32, RP, SA_SAVED, TL, RM>, b.blocks[K_PASS_Q]);
+              L("pass_q_a", k_lqx<DT_F32, RP, SA_SAVED, TL>, b.blocks[K_PASS_Q]);
             else if (saved)
-              L("pass_q_a", k_lqx<DT_F32, RP, SA_SAVED, false, RM>, b.blocks[K_PASS_Q]);
+              L("pass_q_a", k_lqx<DT_F32, RP, SA_SAVED, false>, b.blocks[K_PASS_Q]);
             else
               L("pass_q", k_lqx<DT, RP, SA_MERR, false, RM>, b.blocks[K_PASS_Q]);
           } else {
             if (saved && whole)
-              L("pass_q_a", k_lq<DT_F32, RP, SA_SAVED, TL, RM>, b.blocks[K_PASS_Q]);
+              L("pass_q_a", k_lq<DT_F32, RP, SA_SAVED, TL>, b.blocks[K_PASS_Q]);
             else if (saved)
-              L("pass_q_a", k_lq<DT_F32, RP, SA_SAVED, false, RM>, b.blocks[K_PASS_Q]);
+              L("pass_q_a", k_lq<DT_F32, RP, SA_SAVED, false>, b.blocks[K_PASS_Q]);
             else
               L("pass_q", k_lq<DT, RP, SA_MERR, false, RM>, b.blocks[K_PASS_Q]);
           }
@@ -568,6 +571,10 @@ occ_status_t decompress_impl(const float* P, const float* Q, int64_t m, int64_t 
 
 namespace {
 
+// Leading dimension of the compact stored A of a row-sparse step: whole
+// 128-byte lines per row.
+int64_t compact_ld(int64_t cols) { return round_up(cols, 32); }
+
 // Plan of a row-sparse step: the compressed matrix is the n_rows x cols
 // matrix of the listed rows; its workspace regions are those of a dense
 // matrix of that shape, followed by the validated copy of the row list.
@@ -591,6 +598,11 @@ occ_status_t plan_rows(const occ_mat_t* mat, int64_t n_rows, int rank, int iters
   OCC_TRY(plan_batch(&a, 1, rank, iters, flags, nullptr, 0, true, b));
   rows_off = b.ws_needed;
   b.ws_needed += align_up((size_t)n_rows * 4);
+  if (!b.fused) {
+    // large-rank path: the first left product stores A = M + err_prev of the
+    // listed rows here (n_rows x compact_ld), every later pass reads it back
+    b.ws_needed += align_up((size_t)n_rows * compact_ld(mat->cols) * 4);
+  }
   return OCC_OK;
 }
 
@@ -769,6 +781,13 @@ occ_status_t occ_step_rows(const occ_mat_t* mat, const int32_t* rows, int64_t n_
   d.lde_out = (int32_t)a.lde;
   d.ldh = write_mhat ? (int32_t)a.ldh : 0;
   d.rmap = rmap;
+  if (!b.fused) {
+    // stored A compact in the workspace; the reconstruction writes err
+    d.err_out = (float*)((char*)ws + rows_off + align_up((size_t)n_rows * 4));
+    d.lde_out = (int32_t)compact_ld(a.cols);
+    d.err_fin = a.err;
+    d.lde_fin = (int32_t)a.lde;
+  }
   b.vec = aligned(a.M, 16) && a.ldm % (dt == OCC_BF16 ? 8 : 4) == 0 && aligned(a.err, 16) &&
           a.lde % 4 == 0 && (!write_mhat || (aligned(a.M_hat, 16) && a.ldh % 4 == 0));
   d.vec = b.vec ? 1 : 0;

@@ -119,7 +119,8 @@ __device__ __forceinline__ RawA<DT, SA, W> rawa_load(const Desc& d, bool vec, in
                                                     int c_hi) {
   RawA<DT, SA, W> x;
   if (vec && row < d.m && c + W <= c_hi) {
-    const int64_t pr = prow<RM>(d, row);
+    // M and err_prev rows through the row map; the stored A is compact
+    const int64_t pr = SA == SA_SAVED ? (int64_t)row : prow<RM>(d, row);
     if constexpr (SA == SA_SAVED) {
       ld_f<W>(d.err_out + pr * d.lde_out + c, x.e);
       x.m[0] = 0u;
@@ -143,7 +144,7 @@ __device__ __forceinline__ RawA<DT, SA, W> rawa_load(const Desc& d, bool vec, in
     for (int j = 0; j < W; ++j) {
       float v = 0.f;
       if (row < d.m && c + j < c_hi) {
-        const int64_t pr = prow<RM>(d, row);
+        const int64_t pr = SA == SA_SAVED ? (int64_t)row : prow<RM>(d, row);
         if constexpr (SA == SA_SAVED) {
           v = d.err_out[pr * d.lde_out + c + j];
         } else {
@@ -175,11 +176,11 @@ __device__ __forceinline__ float rawa_val(const RawA<DT, SA, W>& x, int j) {
 // Store W values of A over the error buffer (row < m).  Plain stores: the
 // stored A is read back by the next pass, and nontemporal stores measured
 // slower for the whole step.
-template <int W, bool RM = false>
+template <int W>
 __device__ __forceinline__ void a_store(const Desc& d, bool vec, int row, int c, int c_hi,
                                         const float* a) {
   if (row >= d.m) return;
-  float* p = d.err_out + prow<RM>(d, row) * d.lde_out + c;
+  float* p = d.err_out + (int64_t)row * d.lde_out + c;
   if (vec && c + W <= c_hi) {
     st_f<W>(p, a);
   } else {
@@ -250,18 +251,44 @@ struct LPTile {
   static constexpr int BYTES = A_BYTES + M_BYTES;
 };
 
-template <int DT, int SA>
-__device__ __forceinline__ void lp_tile_issue(const Desc& d, int row0, int c0, uint8_t* dst) {
+// Rows of M and err_prev a lane's tile loads read (the tile rows are the same
+// for every K-step of a wave): with the row map, looked up once before the
+// K-loop, so the loop issues nothing but the tile DMA its wait counts assume.
+struct LPRows {
+  int64_t a[4];   // err_prev rows 8q + l / 8
+  int64_t m[4];   // M rows: bf16 16q + l / 4 (q < 2), fp32 as a
+};
+
+template <int DT, bool RM>
+__device__ __forceinline__ LPRows lp_rows(const Desc& d, int row0) {
+  LPRows r{};
+  if constexpr (RM) {
+    const int lane = threadIdx.x & 63, last = d.m - 1;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) r.a[q] = prow<RM>(d, min(row0 + 8 * q + (lane >> 3), last));
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      r.m[q] = DT == DT_BF16 ? (q < 2 ? prow<RM>(d, min(row0 + 16 * q + (lane >> 2), last)) : 0)
+                             : r.a[q];
+  }
+  return r;
+}
+
+template <int DT, int SA, bool RM = false>
+__device__ __forceinline__ void lp_tile_issue(const Desc& d, int row0, int c0, uint8_t* dst,
+                                              const LPRows& pr = LPRows{}) {
   const int lane = threadIdx.x & 63;
   const int last = d.m - 1;
   const float* asrc = SA == SA_SAVED ? d.err_out : d.err_in;
   const int64_t lda = SA == SA_SAVED ? d.lde_out : d.lde_in;
+  // the stored A is compact: only M and err_prev go through the row map
+  constexpr bool MAP = RM && SA != SA_SAVED;
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     // rows 8q .. 8q+7: lane l takes row l / 8, chunk (l % 8) ^ (l / 8)
     const int rr = lane >> 3, ch = (lane & 7) ^ rr;
-    const int row = min(row0 + 8 * q + rr, last);
-    __builtin_amdgcn_global_load_lds((gvoid_t*)(asrc + (int64_t)row * lda + c0 + 4 * ch),
+    const int64_t row = MAP ? pr.a[q] : (int64_t)min(row0 + 8 * q + rr, last);
+    __builtin_amdgcn_global_load_lds((gvoid_t*)(asrc + row * lda + c0 + 4 * ch),
                                      (lvoid_t*)(dst + q * LP_ESLOT), 16, 0, 0);
   }
   if constexpr (SA != SA_SAVED) {
@@ -271,18 +298,18 @@ __device__ __forceinline__ void lp_tile_issue(const Desc& d, int row0, int c0, u
       for (int q = 0; q < 2; ++q) {
         // rows 16q .. 16q+15: lane l takes row l / 4, chunk (l % 4) ^ (l / 16)
         const int rr = lane >> 2, ch = (lane & 3) ^ (rr >> 2);
-        const int row = min(row0 + 16 * q + rr, last);
+        const int64_t row = MAP ? pr.m[q] : (int64_t)min(row0 + 16 * q + rr, last);
         __builtin_amdgcn_global_load_lds(
-            (gvoid_t*)((const uint16_t*)d.M + (int64_t)row * d.ldm + c0 + 8 * ch),
+            (gvoid_t*)((const uint16_t*)d.M + row * d.ldm + c0 + 8 * ch),
             (lvoid_t*)(mdst + q * LP_BSLOT), 16, 0, 0);
       }
     } else {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int rr = lane >> 3, ch = (lane & 7) ^ rr;
-        const int row = min(row0 + 8 * q + rr, last);
+        const int64_t row = MAP ? pr.m[q] : (int64_t)min(row0 + 8 * q + rr, last);
         __builtin_amdgcn_global_load_lds(
-            (gvoid_t*)((const float*)d.M + (int64_t)row * d.ldm + c0 + 4 * ch),
+            (gvoid_t*)((const float*)d.M + row * d.ldm + c0 + 4 * ch),
             (lvoid_t*)(mdst + q * LP_ESLOT), 16, 0, 0);
       }
     }
@@ -354,7 +381,8 @@ __device__ __forceinline__ void lp_tile_store_a(const Desc& d, const uint8_t* sr
   }
 }
 
-// RM (row-sparse step, register form only): rows through the row map.
+// RM (row-sparse step): M and err_prev rows through the row map; the stored A
+// (SA_MERR_SAVE writes it, SA_SAVED reads it) is compact.
 template <int DT, int RP, int SA, bool X3, bool TILES, bool RM = false>
 __device__ __forceinline__ void lp_body(const Desc& d, int b,
                                         std::conditional_t<X3, LPXSmem<RP>, LPSmem<RP>>& sm,
@@ -470,12 +498,12 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b,
   // TILES: A tiles through LDS (the host picks this instance when rows are
   // 16-byte aligned, every K-step is whole and A has a source); else A goes
   // straight into registers.
-  static_assert(!(TILES && RM), "the row map runs on the register form");
   if constexpr (TILES) {
     constexpr int SB = LPTile<DT, SA>::BYTES;
     uint8_t* const wt = tiles + wave * 2 * SB;   // this wave's two stages
     const int wrow0 = rt * L_PROWS + 32 * wave;
-    lp_tile_issue<DT, SA>(d, wrow0, kcol_of(c_lo, ks0, 0, nk), wt);
+    const LPRows prw = lp_rows<DT, RM && SA != SA_SAVED>(d, wrow0);
+    lp_tile_issue<DT, SA, RM>(d, wrow0, kcol_of(c_lo, ks0, 0, nk), wt, prw);
     __syncthreads();
     for (int it = 0; it < nk; ++it) {
       const int kc0 = kcol_of(c_lo, ks0, it, nk);
@@ -485,7 +513,8 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b,
       float a[16];
       lp_tile_read<DT, SA>(cur, li, g, a);
       if constexpr (SA == SA_MERR_SAVE) lp_tile_store_a<DT>(d, cur, wrow0, kc0);
-      if (it + 1 < nk) lp_tile_issue<DT, SA>(d, wrow0, kcol_of(c_lo, ks0, it + 1, nk), wt + ((it + 1) & 1) * SB);
+      if (it + 1 < nk)
+        lp_tile_issue<DT, SA, RM>(d, wrow0, kcol_of(c_lo, ks0, it + 1, nk), wt + ((it + 1) & 1) * SB, prw);
       mfma_step(a, it & 1);
       if (it + 1 < nk) {
 #pragma unroll
@@ -506,7 +535,7 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b,
       float a[16];
 #pragma unroll
       for (int j = 0; j < 16; ++j) a[j] = rawa_val<DT, SA, 16>(ring[0], j);
-      if constexpr (SA == SA_MERR_SAVE) a_store<16, RM>(d, vec, row, kc + 16 * g, c_hi, a);
+      if constexpr (SA == SA_MERR_SAVE) a_store<16>(d, vec, row, kc + 16 * g, c_hi, a);
       mfma_step(a, it & 1);
 #pragma unroll
       for (int x = 0; x < LP_DEPTH; ++x) ring[x] = ring[x + 1];
@@ -546,10 +575,10 @@ __global__ __launch_bounds__(kBlock) void k_lp(OCC_KARGS) {
 }
 
 // -------------------------------------------------------------------------
-// k_lg: Gram partial of 256 rows in fp64.  MODE 0: the rows are P (sum of
-// the left product's column splits, stored to praw).  MODE 1 (second
-// CholeskyQR pass, skipped unless the first pass asked for it): the rows
-// are the first pass's P_hat.  Rows are staged in LDS as doubles, 32 at a
+// k_lg: Gram partial of d.grows rows (256, fewer for short matrices) in
+// fp64.  MODE 0: the rows are P (sum of the left product's column splits,
+// stored to praw).  MODE 1 (second CholeskyQR pass, skipped unless the first
+// pass asked for it): the rows are the first pass's P_hat.  Rows are staged in LDS as doubles, 32 at a
 // time; the upper-triangle 16 x 16 tiles of G (ta <= tb) are shared out
 // over the four waves and accumulated on v_mfma_f64_16x16x4f64, four rows
 // per instruction: lane (q, li) supplies P[row 4s + q][16 ta + li] (A
@@ -600,7 +629,7 @@ __device__ __forceinline__ void lg_body(const Desc& d, int b, LGSmem<RP>& sm) {
   constexpr int E4 = 32 * RP / 4 / kBlock;
   constexpr int LG_PB = 4;
   static_assert(E4 >= 1 && 32 * RP / 4 == E4 * kBlock, "staging layout");
-  const int r_lo = b * L_GROWS, r_hi = min(d.m, r_lo + L_GROWS);
+  const int r_lo = b * d.grows, r_hi = min(d.m, r_lo + d.grows);
   float4 pre[E4][LG_PB];
   auto fetch = [&](int c0) {
 #pragma unroll
@@ -1737,7 +1766,8 @@ __device__ __forceinline__ void lm_body(const Desc& d, int b, LMSmem<RP>& sm) {
           if (WM) store_mhat_nt<OUTBF>(d, pr * d.ldh + col, mh);
           if (WE) {
             const float e = rawa_val<DT, SA, 1>(av[c][v], 0) - mh;
-            __builtin_nontemporal_store(e, d.err_out + pr * d.lde_out + col);
+            __builtin_nontemporal_store(e, RM ? d.err_fin + pr * d.lde_fin + col
+                                              : d.err_out + pr * d.lde_out + col);
           }
         }
       }
@@ -1911,7 +1941,8 @@ __device__ __forceinline__ void lmx_body(const Desc& d, int b, LMXSmem<RP>& sm) 
           if (WM) store_mhat_nt<OUTBF>(d, pr * d.ldh + col, mh);
           if (WE) {
             const float e = rawa_val<DT_F32, SA_SAVED, 1>(av[c][v], 0) - mh;
-            __builtin_nontemporal_store(e, d.err_out + pr * d.lde_out + col);
+            __builtin_nontemporal_store(e, RM ? d.err_fin + pr * d.lde_fin + col
+                                              : d.err_out + pr * d.lde_out + col);
           }
         }
       }

@@ -296,9 +296,9 @@ __device__ __forceinline__ void p_row(const Desc& d, int64_t row, double* x) {
 }
 
 // k_orth16 block b: full Gram, Cholesky (and the second pass when needed),
-// computed identically in every block, then P_hat for rows
-// [b * F_ORTHROWS, (b + 1) * F_ORTHROWS), written to the caller's P and the
-// padded copy.  Block 0 also stores the second-pass decision and the
+// computed identically in every block, then P_hat for the rows of its
+// 128-row chunks (one chunk per block up to 64 blocks, consecutive chunks
+// beyond), written to the caller's P and the padded copy.  Block 0 also stores the second-pass decision and the
 // numeric flags.
 template <int RP>
 __device__ __forceinline__ void orth16_body(const Desc& d, int b, uint32_t* flags, CholSmem& sm) {
@@ -356,23 +356,28 @@ __device__ __forceinline__ void orth16_body(const Desc& d, int b, uint32_t* flag
     if (t < kWave) chol_lanes<RP>(sm.G, d.r, sm.R[1], sm.inv[1], sm.rowbuf, fl);
     __syncthreads();
   }
-  const int64_t row = (int64_t)b * F_ORTHROWS + t;
-  if (t < F_ORTHROWS && row < d.m) {
-    double x[RP];
-    p_row<RP>(d, row, x);
-    solve_row<RP>(x, sm.R[0], sm.inv[0]);
-    if (need) solve_row<RP>(x, sm.R[1], sm.inv[1]);
-    float out[RP];
+  // this block's 128-row chunks: [b per, (b + 1) per) of the nch chunks
+  const int nch = (d.m + F_ORTHROWS - 1) / F_ORTHROWS;
+  const int per = (nch + orth_blocks(d.m) - 1) / orth_blocks(d.m);
+  for (int c = b * per; c < min(nch, (b + 1) * per); ++c) {
+    const int64_t row = (int64_t)c * F_ORTHROWS + t;
+    if (t < F_ORTHROWS && row < d.m) {
+      double x[RP];
+      p_row<RP>(d, row, x);
+      solve_row<RP>(x, sm.R[0], sm.inv[0]);
+      if (need) solve_row<RP>(x, sm.R[1], sm.inv[1]);
+      float out[RP];
 #pragma unroll
-    for (int k = 0; k < RP; ++k) out[k] = (float)x[k];
-    // the padded copy is always written: the reconstruction pass reads it
-    // with 16-byte loads (the caller's P has no alignment guarantee)
+      for (int k = 0; k < RP; ++k) out[k] = (float)x[k];
+      // the padded copy is always written: the reconstruction pass reads it
+      // with 16-byte loads (the caller's P has no alignment guarantee)
 #pragma unroll
-    for (int k = 0; k < RP; k += 4)
-      *(float4*)(d.phat + row * RP + k) = make_float4(out[k], out[k + 1], out[k + 2], out[k + 3]);
+      for (int k = 0; k < RP; k += 4)
+        *(float4*)(d.phat + row * RP + k) = make_float4(out[k], out[k + 1], out[k + 2], out[k + 3]);
 #pragma unroll
-    for (int k = 0; k < RP; ++k)
-      if (k < d.r) d.P[row * d.r + k] = out[k];
+      for (int k = 0; k < RP; ++k)
+        if (k < d.r) d.P[row * d.r + k] = out[k];
+    }
   }
 }
 

@@ -56,12 +56,17 @@ struct Desc {
                          // rank k in row (k % (rp/32)) * 32 + k / (rp/32)
   const int32_t* rmap;   // row-sparse step: row i of the compressed matrix is row rmap[i]
                          // of M, err and M_hat (validated copy in the workspace); else null
+  float* err_fin;        // row-sparse step, padded rank > 16: the caller's error buffer, which
+                         // the reconstruction pass writes (rows through rmap); err_out then
+                         // holds the stored A compactly (n_rows x lde_out) in the workspace
+  int32_t lde_fin;
   // shapes
   int32_t m, n, r;
   int32_t ldm, lde_in, lde_out, ldh;
   int32_t n_pad;
   int32_t sp, p_cols;    // left product: column splits and columns per split (multiple of 32)
   int32_t ng;            // Gram partials (one per block of the Gram kernel)
+  int32_t grows;         // large-rank path: rows per block of the Gram kernel (multiple of 32)
   int32_t sq, q_rows;    // right product: row splits and rows per split
   int32_t blk[K_NUM];    // first block of this matrix in each kernel's grid
   int32_t fused;         // 1: small-rank path (rank padded to <= 16)
@@ -72,7 +77,7 @@ struct Desc {
 
 // Tiling of one matrix (host side).
 struct Tiling {
-  int sp, p_cols, ng, sq, q_rows, n_pad, m_pad, mr;
+  int sp, p_cols, ng, grows, sq, q_rows, n_pad, m_pad, mr;
   int64_t blocks[K_NUM];
 };
 
@@ -95,7 +100,17 @@ constexpr int F_MHCOLS = 128;     // reconstruction: columns per block
 constexpr int F_MHGROUP = 64;     // reconstruction: rows per block step (4 waves x 16 rows)
 constexpr int F_MHBLOCKS = 1024;  // reconstruction: target number of blocks
 constexpr int F_QBLOCKS = 512;    // right product: target number of blocks
-constexpr int F_ORTHROWS = 128;   // Cholesky/P_hat kernel: rows of P_hat per block
+constexpr int F_ORTHROWS = 128;   // Cholesky/P_hat kernel: rows of P_hat per chunk
+// Cholesky/P_hat kernel: blocks per matrix, at most.  Every block sums all
+// Gram partials (and, for a second CholeskyQR pass, forms the second Gram over
+// all rows), so the block count is capped to keep that work linear in m; a
+// block then forms P_hat for several consecutive 128-row chunks.
+constexpr int F_ORTHBLOCKS = 64;
+__host__ __device__ inline int orth_blocks(int64_t m) {
+  const int64_t chunks = (m + F_ORTHROWS - 1) / F_ORTHROWS;
+  return (int)(chunks < F_ORTHBLOCKS ? chunks : F_ORTHBLOCKS);
+}
+
 // Large-rank path (padded rank 32, 64, 128): tile constants shared with
 // kernels_large.hpp.
 constexpr int L_PROWS = 128;      // left product: rows per block (4 waves x 32)
@@ -106,7 +121,7 @@ constexpr int L_QG = 8;           // right product: rows per LDS stage
 constexpr int64_t L_SPLIT_BLOCKS = 1024;  // split products: blocks over the whole batch
 constexpr int64_t L_MIN_COLS = 1024;      // left product: columns per split, at least
 constexpr int64_t L_MIN_ROWS = 1024;      // right product: rows per split, at least
-constexpr int64_t L_MIN_SPLIT = 512;      // columns / rows per split, at least
+constexpr int64_t L_MIN_NARROW = 256;     // the same for matrices that cannot fill a round
 // right product: columns per lane and per block
 __host__ __device__ constexpr int lq_cpl(int rp) { return rp >= 128 ? 1 : 128 / rp; }
 __host__ __device__ constexpr int lq_block_cols(int rp) { return 128 * lq_cpl(rp); }
@@ -152,7 +167,7 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0,
     t.mr = (int)round_up(cdiv(m, rbm), F_MHGROUP);
     t.blocks[K_QPAD] = cdiv((int64_t)t.n_pad * rp, kBlock);
     t.blocks[K_PASS_P] = p_blocks;
-    t.blocks[K_PGRAM] = cdiv(m, F_ORTHROWS);
+    t.blocks[K_PGRAM] = orth_blocks(m);
     t.blocks[K_PASS_Q] = col_tiles * t.sq;
     t.blocks[K_QRED] = cdiv(n * rp, kBlock);
     t.blocks[K_MHAT] = ctm * cdiv(m, t.mr);
@@ -173,19 +188,33 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0,
   const int64_t target = target_of(L_SPLIT_BLOCKS, sl.p);
   const int64_t target_q = target_of(L_SPLIT_BLOCKS, sl.q);
   const int64_t target_m = target_of(2 * L_SPLIT_BLOCKS, sl.m);
-  // left product: 128-row tiles, columns split
+  // left product: 128-row tiles, columns split, splits at least L_MIN_COLS
+  // wide -- narrower, down to L_MIN_NARROW, while this matrix's blocks would
+  // leave its share of one round of resident blocks partly empty (a matrix of
+  // few rows, e.g. the rows of a row-sparse step)
   const int64_t row_tiles = cdiv(m, L_PROWS);
-  const int64_t sp = clamp64(cdiv(target, row_tiles), 1, cdiv(n, L_MIN_COLS));
+  int64_t min_cols = L_MIN_COLS;
+  auto sp_of = [&](int64_t mc) { return clamp64(cdiv(target, row_tiles), 1, cdiv(n, mc)); };
+  while (min_cols > L_MIN_NARROW && row_tiles * sp_of(min_cols) < (int64_t)(share * (double)sl.p))
+    min_cols /= 2;
+  const int64_t sp = sp_of(min_cols);
   t.p_cols = (int)round_up(cdiv(n, sp), L_KC);
   t.sp = (int)cdiv(n, t.p_cols);
-  t.ng = (int)cdiv(m, L_GROWS);
+  // Gram partials: L_GROWS rows per block, fewer (down to 32) for a matrix
+  // too short to give its share of about 128 blocks (a row-sparse step's
+  // rows); every block also sums the column splits of its rows
+  const int64_t g_want = std::max<int64_t>(1, (int64_t)(share * 128.0));
+  t.grows = (int)clamp64(round_up(cdiv(m, g_want), 32), 32, L_GROWS);
+  t.ng = (int)cdiv(m, t.grows);
   // right product: column tiles, rows split
   const int64_t ctq = cdiv(n, lq_block_cols(rp));
-  // splits of L_MIN_ROWS rows, or half that when those would leave this
-  // matrix's share of one round of resident blocks partly empty (a single
-  // 51200 x 3072 matrix at rank 64: 600 of 1024 slots; 0.24 -> 0.20 ms)
-  const int64_t min_rows =
-      ctq * cdiv(m, L_MIN_ROWS) < (int64_t)(share * (double)sl.q) ? L_MIN_ROWS / 2 : L_MIN_ROWS;
+  // splits of L_MIN_ROWS rows, halved (down to L_MIN_NARROW) while they
+  // would leave this matrix's share of one round of resident blocks partly
+  // empty (a single 51200 x 3072 matrix at rank 64: 600 of 1024 slots, so
+  // 512-row splits; 0.24 -> 0.20 ms)
+  int64_t min_rows = L_MIN_ROWS;
+  while (min_rows > L_MIN_NARROW && ctq * cdiv(m, min_rows) < (int64_t)(share * (double)sl.q))
+    min_rows /= 2;
   const int64_t sq = clamp64(cdiv(target_q, ctq), 1, cdiv(m, min_rows));
   // splits start on 16-row boundaries: the bf16 right product walks 16-row
   // groups, and its P_hat^T parts are stored in 16-row tiles

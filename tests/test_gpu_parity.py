@@ -143,6 +143,26 @@ def test_ill_conditioned_iterates_second_pass(rank, iters, ratio):
     assert_parity(res, "f32", f"geometric {ratio}^-j r{rank} t{iters}")
 
 
+@pytest.mark.parametrize("shape,rank,iters", [((20000, 96), 16, 1), ((9000, 130), 8, 2),
+                                              ((8193, 64), 4, 1)])
+def test_tall_small_rank_chunked_orthogonalisation(shape, rank, iters):
+    """More than 64 x 128 rows at rank <= 16: the orthogonalisation kernel
+    runs 64 blocks, each forming P_hat for several consecutive 128-row chunks
+    (8193 rows: one block takes the single row of the last chunk)."""
+    w = Workload(94, "tall", (shape,), "f32", rank, iters, 2, "gauss", std=1.0)
+    res, _, _ = run_workload(w, 2)
+    assert_parity(res, "f32", f"tall {shape[0]}x{shape[1]} r{rank} t{iters}")
+
+
+def test_tall_small_rank_second_pass():
+    """A tall matrix with ill-conditioned iterates (geometric spectrum 1.2^-j,
+    rank 16, t = 2): the second CholeskyQR pass runs with capped blocks."""
+    w = Workload(95, "geom_tall", ((12000, 64),), "f32", 16, 2, 2, "geom", signal_rank=24,
+                 noise=1.2)
+    res, _, _ = run_workload(w, 2)
+    assert_parity(res, "f32", "geometric 1.2^-j 12000x64 r16 t2")
+
+
 @pytest.mark.parametrize("shape,rank", [((1, 1), 1), ((5, 3), 3), ((64, 1), 1), ((1, 100), 1),
                                         ((65, 33), 8), ((3, 200), 2)])
 def test_tiny_shapes(shape, rank):
