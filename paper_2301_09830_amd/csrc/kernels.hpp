@@ -216,14 +216,15 @@ constexpr double kSecondPassCond = 1e3;
 // 2^-16 |v|) in qbf, transposed so that the left product stages 32 columns
 // of a rank row with 16-byte copies: rank k goes to row (k % NU) * 32 + k / NU,
 // NU = RP / 32, the order in which that kernel's lanes read them.  The
-// transpose goes through LDS, so qbf is written in 16-byte runs.
+// transpose goes through LDS, so each qbf row is written in 64-byte runs.
 // k_qpadl covers all n_pad columns (zeros past n); k_qredl sums the row-split
 // partials (fixed order) for the n real columns and also writes the caller's Q.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ uint16_t bf16_bits(__bf16 h) { return __builtin_bit_cast(uint16_t, h); }
 
-constexpr int QT_COLS = 8;                  // columns per block
+constexpr int QT_COLS = 32;                 // columns per block
 constexpr int QT_P = QT_COLS;               // LDS pitch (bf16) of a transposed rank row
+constexpr int QT_CH = QT_COLS / 8;          // 16-byte chunks of a transposed rank row
 
 template <int RP>
 struct QTSmem {
@@ -265,10 +266,11 @@ __device__ __forceinline__ void qtile_body(const Desc& d, int b, QTSmem<RP>& sm)
   }
   if (!d.qbf) return;
   __syncthreads();
-  // 2 x RP rows of 8 columns, one 16-byte chunk each
-  for (int f = threadIdx.x; f < 2 * RP; f += kBlock) {
-    const int h = f / RP, prow = f % RP, part = 0;
-    const int c = c0;
+  // 2 x RP rows of QT_COLS columns, QT_CH 16-byte chunks each
+  for (int f = threadIdx.x; f < 2 * RP * QT_CH; f += kBlock) {
+    const int h = f / (RP * QT_CH), prow = (f / QT_CH) % RP, part = f % QT_CH;
+    const int c = c0 + 8 * part;
+    if (c >= c_end) continue;
     if (c + 8 <= c_end) {
       *(uint4*)(d.qbf + ((int64_t)h * RP + prow) * d.n_pad + c) = *(const uint4*)(&sm.t[h][prow * QT_P + 8 * part]);
     } else {
@@ -310,8 +312,9 @@ __global__ __launch_bounds__(kBlock) void k_err_update(Desc d) {
   }
 }
 
-// Copy descriptor chunks passed by value into the workspace table.
-constexpr int kTableChunk = 4;
+// Copy descriptor chunks passed by value into the workspace table (12
+// descriptors, 3.3 KB of kernel arguments per launch).
+constexpr int kTableChunk = 12;
 struct TableChunk {
   Desc d[kTableChunk];
 };

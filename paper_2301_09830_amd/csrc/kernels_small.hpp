@@ -125,6 +125,7 @@ struct CholSmem {
   double inv[2][16];          // 1 / R[k][k], zero for a dependent column
   double rowbuf[2][16];       // pivot row of the current Schur complement
   double rows[CH_CHUNK * 16];
+  double T[16 * 16];          // P_hat = P T (row-major)
   uint32_t need;
 };
 
@@ -296,7 +297,7 @@ __device__ __forceinline__ void p_row(const Desc& d, int64_t row, double* x) {
 }
 
 // k_orth16 block b: full Gram, Cholesky (and the second pass when needed),
-// computed identically in every block, then P_hat for the rows of its
+// computed identically in every block, then P_hat = P T for the rows of its
 // 128-row chunks (one chunk per block up to 64 blocks, consecutive chunks
 // beyond), written to the caller's P and the padded copy.  Block 0 also stores the second-pass decision and the
 // numeric flags.
@@ -356,27 +357,55 @@ __device__ __forceinline__ void orth16_body(const Desc& d, int b, uint32_t* flag
     if (t < kWave) chol_lanes<RP>(sm.G, d.r, sm.R[1], sm.inv[1], sm.rowbuf, fl);
     __syncthreads();
   }
+  // The substitution x -> x R1^-1 (R2^-1) is linear, so P_hat = P T with row
+  // i of T the image of the unit row e_i (upper triangular; a dependent
+  // column's inverse diagonal is zero, so its column of T is zero): RP
+  // threads form T in fp64, then every row of P_hat is a product with T,
+  // TPR threads per row each forming OPT of its columns.
+  if (t < RP) {
+    double x[RP];
+#pragma unroll
+    for (int k = 0; k < RP; ++k) x[k] = (k == t) ? 1.0 : 0.0;
+    solve_row<RP>(x, sm.R[0], sm.inv[0]);
+    if (need) solve_row<RP>(x, sm.R[1], sm.inv[1]);
+#pragma unroll
+    for (int k = 0; k < RP; ++k) sm.T[t * RP + k] = x[k];
+  }
+  __syncthreads();
+  constexpr int OPT = RP >= 16 ? RP / 8 : 1;   // columns of P_hat per thread
+  constexpr int TPR = RP / OPT;                // threads per row
+  static_assert(F_ORTHROWS * TPR <= CH_THREADS, "a chunk's rows at once");
+  const int i = t / TPR, j0 = (t % TPR) * OPT;
+  double tc[OPT][RP];   // this thread's columns of T
+#pragma unroll
+  for (int q = 0; q < OPT; ++q)
+#pragma unroll
+    for (int k = 0; k < RP; ++k) tc[q][k] = sm.T[k * RP + j0 + q];
   // this block's 128-row chunks: [b per, (b + 1) per) of the nch chunks
   const int nch = (d.m + F_ORTHROWS - 1) / F_ORTHROWS;
   const int per = (nch + orth_blocks(d.m) - 1) / orth_blocks(d.m);
   for (int c = b * per; c < min(nch, (b + 1) * per); ++c) {
-    const int64_t row = (int64_t)c * F_ORTHROWS + t;
-    if (t < F_ORTHROWS && row < d.m) {
+    const int64_t row = (int64_t)c * F_ORTHROWS + i;
+    if (i < F_ORTHROWS && row < d.m) {
       double x[RP];
       p_row<RP>(d, row, x);
-      solve_row<RP>(x, sm.R[0], sm.inv[0]);
-      if (need) solve_row<RP>(x, sm.R[1], sm.inv[1]);
-      float out[RP];
+      float out[OPT];
 #pragma unroll
-      for (int k = 0; k < RP; ++k) out[k] = (float)x[k];
+      for (int q = 0; q < OPT; ++q) {
+        double acc = 0.0;
+#pragma unroll
+        for (int k = 0; k < RP; ++k) acc = fma(x[k], tc[q][k], acc);
+        out[q] = (float)acc;
+      }
       // the padded copy is always written: the reconstruction pass reads it
       // with 16-byte loads (the caller's P has no alignment guarantee)
+      if constexpr (OPT == 2)
+        *(float2*)(d.phat + row * RP + j0) = make_float2(out[0], out[1]);
+      else
+        d.phat[row * RP + j0] = out[0];
 #pragma unroll
-      for (int k = 0; k < RP; k += 4)
-        *(float4*)(d.phat + row * RP + k) = make_float4(out[k], out[k + 1], out[k + 2], out[k + 3]);
-#pragma unroll
-      for (int k = 0; k < RP; ++k)
-        if (k < d.r) d.P[row * d.r + k] = out[k];
+      for (int q = 0; q < OPT; ++q)
+        if (j0 + q < d.r) d.P[row * d.r + j0 + q] = out[q];
     }
   }
 }

@@ -224,14 +224,14 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0,
   const int64_t ctm = cdiv(n, lm_block_cols(rp));
   const int64_t rbm = clamp64(cdiv(target_m, ctm), 1, cdiv(m, 32));
   t.mr = (int)round_up(cdiv(m, rbm), 32);
-  t.blocks[K_QPAD] = cdiv(t.n_pad, 8);    // 8-column tiles (k_qpadl)
+  t.blocks[K_QPAD] = cdiv(t.n_pad, 32);   // 32-column tiles (k_qpadl)
   t.blocks[K_PASS_P] = row_tiles * t.sp;
   t.blocks[K_PGRAM] = t.ng;
   t.blocks[K_GSUM] = cdiv((int64_t)rp * rp, kBlock / 8);   // 32 entries per block
   t.blocks[K_GRAM2] = t.ng;
   t.blocks[K_APPLY] = cdiv(m, L_AROWS);
   t.blocks[K_PASS_Q] = ctq * t.sq;
-  t.blocks[K_QRED] = cdiv(n, 8);          // 8-column tiles (k_qredl)
+  t.blocks[K_QRED] = cdiv(n, 32);         // 32-column tiles (k_qredl)
   t.blocks[K_MHAT] = ctm * cdiv(m, t.mr);
   return t;
 }
