@@ -381,8 +381,16 @@ def main() -> int:
     if args.write_profiles:
         from workloads import WORKLOADS
         w = WORKLOADS[args.workload]
-        paths = write_profiles(w.name, *args.write_profiles, json.loads(args.profile_commands),
-                               w.elements, 2 if w.m_dtype == "bf16" else 4, mfma_dir=args.mfma_dir,
+        name, elements = w.name, w.elements
+        if args.rows:
+            # the rows the row-sparse step touches: the union over the inputs
+            import numpy as np
+            live = np.zeros(w.shapes[0][0], dtype=bool)
+            for s in range(args.inputs or w.steps):
+                live |= (w.matrix(s, 0) != 0).any(axis=1)
+            name, elements = w.name + "_rows", int(live.sum()) * w.shapes[0][1]
+        paths = write_profiles(name, *args.write_profiles, json.loads(args.profile_commands),
+                               elements, 2 if w.m_dtype == "bf16" else 4, mfma_dir=args.mfma_dir,
                                streaming_only=w.rank > 16)
         print("\n".join(paths))
         return 0

@@ -133,6 +133,29 @@ __device__ __forceinline__ int find_matrix(const Desc* __restrict__ table, int c
 
 #define OCC_KARGS const Desc* __restrict__ table, int count, Desc single
 
+// Tile index of a block of a kernel whose neighbouring tiles share an operand
+// slice (the Q columns of a left-product split, the P_hat rows of a
+// right-product split or reconstruction row block).  Workgroups are dealt to
+// the 8 XCDs round-robin (workgroup b to XCD b % 8), each XCD with its own L2;
+// renumbering so that XCD x takes the contiguous tile range
+// [x G8 / 8, (x + 1) G8 / 8) (G8 = the grid rounded down to a multiple of 8;
+// the last G - G8 blocks keep their index) keeps the tiles that run on one
+// XCD on few slices.  A bijection of [0, G): results do not change.
+__device__ __forceinline__ int xcd_tile() {
+  const int g8 = (int)gridDim.x & ~7, b = (int)blockIdx.x;
+  return b < g8 ? (b & 7) * (g8 >> 3) + (b >> 3) : b;
+}
+
+#define OCC_DISPATCH_X(KIND, BODY)                                      \
+  if (count == 1) {                                                     \
+    BODY(single, xcd_tile());                                           \
+  } else {                                                              \
+    const int v_ = xcd_tile();                                          \
+    const int j_ = find_matrix(table, count, KIND, v_);                 \
+    const Desc& d_ = table[j_];                                         \
+    BODY(d_, v_ - d_.blk[KIND]);                                        \
+  }
+
 // ---------------------------------------------------------------------------
 // Warm-start Q -> padded layout qpad[n_pad][rp] (zeros beyond n and rank).
 // ---------------------------------------------------------------------------

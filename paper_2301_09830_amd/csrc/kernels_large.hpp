@@ -274,6 +274,15 @@ __device__ __forceinline__ LPRows lp_rows(const Desc& d, int row0) {
   return r;
 }
 
+// Cache policy of tile loads (2: non-temporal) for data read once in whole
+// lines: the stored A of later passes and fp32 M.  err is read and then
+// overwritten by the stored A in the same lines, and a bf16 K-step reads half
+// of each M line (the other half comes with the next K-step), so both keep
+// the default policy.  Measured (same session): the later rank-128 left
+// product 507 -> 471 us, the stage matrices' 801 -> 747 us and their first
+// pass 2457 -> 2408 us, the embedding's first pass 414 -> 396 us; bf16 M
+// non-temporal made the rank-128 first pass 1161 -> 1267 us.
+constexpr int LP_NT = 2;
 template <int DT, int SA, bool RM = false>
 __device__ __forceinline__ void lp_tile_issue(const Desc& d, int row0, int c0, uint8_t* dst,
                                               const LPRows& pr = LPRows{}) {
@@ -289,7 +298,8 @@ __device__ __forceinline__ void lp_tile_issue(const Desc& d, int row0, int c0, u
     const int rr = lane >> 3, ch = (lane & 7) ^ rr;
     const int64_t row = MAP ? pr.a[q] : (int64_t)min(row0 + 8 * q + rr, last);
     __builtin_amdgcn_global_load_lds((gvoid_t*)(asrc + row * lda + c0 + 4 * ch),
-                                     (lvoid_t*)(dst + q * LP_ESLOT), 16, 0, 0);
+                                     (lvoid_t*)(dst + q * LP_ESLOT), 16, 0,
+                                     SA == SA_SAVED ? LP_NT : 0);
   }
   if constexpr (SA != SA_SAVED) {
     uint8_t* mdst = dst + LPTile<DT, SA>::A_BYTES;
@@ -310,7 +320,7 @@ __device__ __forceinline__ void lp_tile_issue(const Desc& d, int row0, int c0, u
         const int64_t row = MAP ? pr.m[q] : (int64_t)min(row0 + 8 * q + rr, last);
         __builtin_amdgcn_global_load_lds(
             (gvoid_t*)((const float*)d.M + row * d.ldm + c0 + 4 * ch),
-            (lvoid_t*)(mdst + q * LP_ESLOT), 16, 0, 0);
+            (lvoid_t*)(mdst + q * LP_ESLOT), 16, 0, LP_NT);
       }
     }
   }
@@ -1350,12 +1360,12 @@ __global__ __launch_bounds__(kBlock) void k_lq(OCC_KARGS) {
     static_assert(DT == DT_F32 && SA == SA_SAVED, "tiles hold the stored fp32 A");
     __shared__ __attribute__((aligned(16))) uint8_t tiles[LQTile<RP>::AST * LQTile<RP>::STAGE];
 #define B_(d, b) lq_tiles_body<RP>(d, b, tiles)
-    OCC_DISPATCH(K_PASS_Q, B_)
+    OCC_DISPATCH_X(K_PASS_Q, B_)
 #undef B_
   } else {
     __shared__ __attribute__((aligned(16))) LQSmem<RP> sm;
 #define B_(d, b) lq_body<DT, RP, SA, RM>(d, b, sm)
-    OCC_DISPATCH(K_PASS_Q, B_)
+    OCC_DISPATCH_X(K_PASS_Q, B_)
 #undef B_
   }
 }
@@ -1650,7 +1660,7 @@ __global__ __launch_bounds__(kBlock) void k_lqx(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) LQXSmem<RP> sm;
   __shared__ __attribute__((aligned(16))) uint8_t tiles[TILES ? 4 * LQXTile<RP>::AST * LQXTile<RP>::BYTES : 16];
 #define B_(d, b) lqx_body<DT, RP, SA, TILES, RM>(d, b, sm, tiles)
-  OCC_DISPATCH(K_PASS_Q, B_)
+  OCC_DISPATCH_X(K_PASS_Q, B_)
 #undef B_
 }
 
@@ -1791,7 +1801,7 @@ template <int DT, int RP, int SA, int SRC, bool WM, bool WE, bool OUTBF = false,
 __global__ __launch_bounds__(kBlock) void k_ml(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) LMSmem<RP> sm;
 #define B_(d, b) lm_body<DT, RP, SA, SRC, WM, WE, OUTBF, RM>(d, b, sm)
-  OCC_DISPATCH(K_MHAT, B_)
+  OCC_DISPATCH_X(K_MHAT, B_)
 #undef B_
 }
 
@@ -1956,7 +1966,7 @@ template <int RP, int SRC, bool WM, bool WE, bool OUTBF = false, bool RM = false
 __global__ __launch_bounds__(kBlock) void k_mlx(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) LMXSmem<RP> sm;
 #define B_(d, b) lmx_body<RP, SRC, WM, WE, OUTBF, RM>(d, b, sm)
-  OCC_DISPATCH(K_MHAT, B_)
+  OCC_DISPATCH_X(K_MHAT, B_)
 #undef B_
 }
 
