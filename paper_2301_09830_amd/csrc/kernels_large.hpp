@@ -719,9 +719,12 @@ __global__ __launch_bounds__(kBlock) void k_lg(OCC_KARGS) {
 // upper triangle only, held in LDS).  Step j:
 //   1. wave 0 factors the diagonal tile W_jj = R_jj^T R_jj with the
 //      right-looking column recurrence (Cholesky of W_jj together with the
-//      column recurrence of its inverse factor; row j of W and column j of
-//      T shared through LDS), giving T_jj = R_jj^-1 and the pivots, while
-//      the other waves finish column block j-1 of T (step 4);
+//      column recurrence of its inverse factor; each lane reads the pivot
+//      row of W and the pivot column of T from the owning lanes' registers
+//      with cross-lane shuffles, so a column step waits for one round of
+//      shuffles instead of an LDS write and read), giving T_jj = R_jj^-1
+//      and the pivots, while the other waves finish column block j-1 of T
+//      (step 4);
 //   2. row panel R_jk = T_jj^T W_jk (k > j) and U_kj = R_kj T_jj (k < j);
 //   3. trailing update W_kl -= R_jk^T R_jl (j < k <= l);
 //   4. T_ij = -sum_{k=i..j-1} T_ik U_kj (i < j), from T R = I.
@@ -747,12 +750,20 @@ template <int RP>
 struct LCSmem {
   double W[lc_ntiles(RP / 16)][256];   // G, then R (row panels) and U
   double T[lc_ntiles(RP / 16)][256];
-  double rowbuf[2][16];
-  double colbuf[2][16];
   double sdiag[RP];    // sqrt of each pivot (0 when dependent)
   int dep[RP];
   double thr;
 };
+
+// 1/v for v > 0: hardware estimate refined by two Newton steps
+// (y <- y + y (1 - v y)), accurate to an ulp or two.
+__device__ __forceinline__ double rcp_nr(double v) {
+  double y = __builtin_amdgcn_rcp(v);
+  double e = fma(-v, y, 1.0);
+  y = fma(y, e, y);
+  e = fma(-v, y, 1.0);
+  return fma(y, e, y);
+}
 
 // D (+)= sum over 16 of A * B for one tile product; fa(s) / fb(s) give the
 // lane's A / B operand of step s.
@@ -785,19 +796,32 @@ __device__ __forceinline__ void lchol_body(const Desc& d, uint32_t* flags, LCSme
     for (int c = 0; c < 4; ++c) X[lc_sw(4 * c + q, li)] = v[c];
   };
 
-  // G's upper tiles into LDS
-  for (int idx = t; idx < NUT * 256; idx += LC_THREADS) {
-    const int u = idx >> 8, e = idx & 255, rr = e >> 4, cc = e & 15;
-    int a = 0, rem = u;
-    while (rem >= NB - a) { rem -= NB - a; ++a; }
-    sm.W[u][lc_sw(rr, cc)] = G[(16 * a + rr) * RP + 16 * (a + rem) + cc];
+  // G's upper tiles into LDS, all of a thread's loads in flight at once
+  constexpr int GL = (NUT * 256 + LC_THREADS - 1) / LC_THREADS;
+  double gl[GL];
+#pragma unroll
+  for (int x = 0; x < GL; ++x) {
+    const int idx = t + LC_THREADS * x;
+    gl[x] = 0.0;
+    if (idx < NUT * 256) {
+      const int u = idx >> 8, e = idx & 255, rr = e >> 4, cc = e & 15;
+      int a = 0, rem = u;
+      while (rem >= NB - a) { rem -= NB - a; ++a; }
+      gl[x] = G[(16 * a + rr) * RP + 16 * (a + rem) + cc];
+    }
   }
+#pragma unroll
+  for (int x = 0; x < GL; ++x) {
+    const int idx = t + LC_THREADS * x;
+    if (idx < NUT * 256) sm.W[idx >> 8][lc_sw((idx & 255) >> 4, idx & 15)] = gl[x];
+  }
+  __syncthreads();
   if (t < kWave) {
-    // max of diag(G) over the first wave (max is order-independent)
+    // max of diag(G) over the first wave (max is order-independent), from LDS
     double mx = 0.0;
     int nonfinite = 0;
     for (int j = t; j < RP; j += kWave) {
-      const double gv = G[j * RP + j];
+      const double gv = sm.W[lc_ut(NB, j >> 4, j >> 4)][lc_sw(j & 15, j & 15)];
       if (!isfinite(gv)) nonfinite = 1;
       if (gv > mx) mx = gv;
     }
@@ -843,28 +867,21 @@ __device__ __forceinline__ void lchol_body(const Desc& d, uint32_t* flags, LCSme
       bool mydep = true;
 #pragma unroll 1
       for (int jv = 0; jv < 4; ++jv) {
-        // (register arrays need compile-time indices: W[jv] by selects)
 #pragma unroll
         for (int jq = 0; jq < 4; ++jq) {
-          const int jj = 4 * jv + jq, buf = jq & 1;
-          if (q == jq) {
-            double w = W[0];
+          const int jj = 4 * jv + jq;
+          // Row jj of W is W[jv] of lanes (jq, 0..15); column jj of T is T[v]
+          // of lanes (q, jj).  Read straight from those lanes' registers.
+          double w = W[0];
 #pragma unroll
-            for (int v = 1; v < 4; ++v) w = (jv == v) ? W[v] : w;
-            sm.rowbuf[buf][li] = w;   // row jj of W
-          }
-          if (li == jj) {
-#pragma unroll
-            for (int v = 0; v < 4; ++v) sm.colbuf[buf][4 * v + q] = T[v];   // column jj of T
-          }
-          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-          const double piv = sm.rowbuf[buf][jj];
-          const double wk = sm.rowbuf[buf][li];
+          for (int v = 1; v < 4; ++v) w = (jv == v) ? W[v] : w;
+          const double piv = __shfl(w, 16 * jq + jj);
+          const double wk = __shfl(w, 16 * jq + li);
           double wi[4], tl[4];
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
-            wi[v] = sm.rowbuf[buf][4 * v + q];
-            tl[v] = sm.colbuf[buf][4 * v + q];
+            wi[v] = __shfl(w, 16 * jq + 4 * v + q);
+            tl[v] = __shfl(T[v], 16 * q + jj);
           }
           const bool dep = (16 * j + jj >= r) || (piv <= thr);
           if (li == jj) {
@@ -872,7 +889,7 @@ __device__ __forceinline__ void lchol_body(const Desc& d, uint32_t* flags, LCSme
             mydep = dep;
           }
           if (!dep && li > jj) {
-            const double ip = 1.0 / piv;
+            const double ip = rcp_nr(piv);
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
               const int i = 4 * v + q;
@@ -885,10 +902,11 @@ __device__ __forceinline__ void lchol_body(const Desc& d, uint32_t* flags, LCSme
           }
         }
       }
-      const double sq = mydep ? 0.0 : sqrt(mypiv);
+      const double isq = mydep ? 0.0 : rsqrt_nr(mypiv);
+      const double sq = mypiv * isq;   // sqrt of the pivot (0 when dependent)
       double* Td = sm.T[lc_ut(NB, j, j)];
 #pragma unroll
-      for (int v = 0; v < 4; ++v) Td[lc_sw(4 * v + q, li)] = (4 * v + q <= li && !mydep) ? T[v] / sq : 0.0;
+      for (int v = 0; v < 4; ++v) Td[lc_sw(4 * v + q, li)] = (4 * v + q <= li && !mydep) ? T[v] * isq : 0.0;
       if (q == 0) {
         sm.sdiag[16 * j + li] = sq;
         sm.dep[16 * j + li] = mydep ? 1 : 0;
