@@ -123,7 +123,6 @@ struct CholSmem {
   double G[16 * 16];
   double R[2][16 * 16];       // factors of the two passes (upper triangle, row-major)
   double inv[2][16];          // 1 / R[k][k], zero for a dependent column
-  double rowbuf[2][16];       // pivot row of the current Schur complement
   double rows[CH_CHUNK * 16];
   double T[16 * 16];          // P_hat = P T (row-major)
   uint32_t need;
@@ -139,11 +138,6 @@ __device__ __forceinline__ double rsqrt_nr(double v) {
   return fma(0.5 * y, e, y);
 }
 
-// LDS writes of this wave are complete before its next LDS read is issued
-// (LDS executes one wave's instructions in order; this keeps the compiler
-// from moving the reads above the writes and waits for the writes).
-__device__ __forceinline__ void wave_lds_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
-
 struct CholInfo {
   uint32_t defmask;   // dependent columns
   double pmax, pmin;  // extreme pivots (squared diagonal of R) over independent columns
@@ -153,15 +147,18 @@ struct CholInfo {
 // row-major), by one wave; R (upper triangle, zero below) and the inverse
 // diagonal go to LDS.  Right-looking on the upper triangle: lane slot
 // (lane, q) owns entry e = lane + 64 q = (i, j) of the Schur complement; at
-// step k the owners of row k publish it, every slot reads the pivot and its
-// two row-k factors, and entries with k < i <= j are updated.  Columns >= r
+// step k every slot reads the pivot and its two row-k factors straight from
+// the registers of the lanes owning row k (cross-lane shuffles: row k is
+// slot k RP / 64 of lanes k RP % 64 .. + RP - 1), and entries with
+// k < i <= j are updated.  Columns >= r
 // are padding; a pivot <= kPivotTol * max diag(G) marks its column
 // dependent: that row of R is the unit row, its inverse diagonal is zero (the
 // column of P_hat is zero) and later steps ignore it.  NaN pivots are not
 // dependent: they propagate like the data.
 template <int RP>
 __device__ __forceinline__ CholInfo chol_lanes(const double* G, int r, double* R, double* inv,
-                                              double (*rowbuf)[16], uint32_t* flags) {
+                                              uint32_t* flags) {
+  static_assert(64 % RP == 0, "a row of the Schur complement lies in one slot");
   constexpr int NE = (RP * RP + kWave - 1) / kWave;
   const int lane = threadIdx.x & 63;
   double w[NE];
@@ -190,17 +187,15 @@ __device__ __forceinline__ CholInfo chol_lanes(const double* G, int r, double* R
   o.pmin = 1e308;
 #pragma unroll
   for (int k = 0; k < RP; ++k) {
-    double* rb = rowbuf[k & 1];
-#pragma unroll
-    for (int q = 0; q < NE; ++q)
-      if (up[q] && ei[q] == k) rb[ej[q]] = w[q];
-    wave_lds_sync();
-    const double piv = rb[k];
+    // entry (k, x) of the Schur complement: slot k RP / 64 of lane k RP % 64 + x
+    const double wk = w[(k * RP) / kWave];
+    const int base = (k * RP) % kWave;
+    const double piv = __shfl(wk, base + k);
     double ri[NE], rj[NE];
 #pragma unroll
     for (int q = 0; q < NE; ++q) {
-      ri[q] = rb[ei[q] < RP ? ei[q] : 0];
-      rj[q] = rb[ej[q]];
+      ri[q] = __shfl(wk, base + (ei[q] < RP ? ei[q] : 0));
+      rj[q] = __shfl(wk, base + ej[q]);
     }
     const bool dep = (k >= r) || (piv <= thr);
     o.defmask |= dep ? (1u << k) : 0u;
@@ -307,7 +302,7 @@ __device__ __forceinline__ void orth16_body(const Desc& d, int b, uint32_t* flag
   uint32_t* fl = (b == 0) ? flags : nullptr;
   gram_sum_all<RP>(d.gpart, d.ng, sm, sm.G);
   if (t < kWave) {
-    const CholInfo o = chol_lanes<RP>(sm.G, d.r, sm.R[0], sm.inv[0], sm.rowbuf, fl);
+    const CholInfo o = chol_lanes<RP>(sm.G, d.r, sm.R[0], sm.inv[0], fl);
     const uint32_t need = needs_second_pass(o);
     if (t == 0) {
       if (b == 0) d.info[0] = need;
@@ -354,7 +349,7 @@ __device__ __forceinline__ void orth16_body(const Desc& d, int b, uint32_t* flag
       sm.G[pl_ * RP + pk_] = sacc;
     }
     __syncthreads();
-    if (t < kWave) chol_lanes<RP>(sm.G, d.r, sm.R[1], sm.inv[1], sm.rowbuf, fl);
+    if (t < kWave) chol_lanes<RP>(sm.G, d.r, sm.R[1], sm.inv[1], fl);
     __syncthreads();
   }
   // The substitution x -> x R1^-1 (R2^-1) is linear, so P_hat = P T with row
