@@ -224,8 +224,8 @@ def profile_name(kname: str) -> str | None:
     base = kname.split("(")[0].replace("void ", "").replace("occ::", "").strip()
     short = base.split("<")[0]
     args = [a.strip() for a in base[len(short) + 1:-1].split(",")] if "<" in base else []
-    fixed = {"k_pm": "pass_p", "k_qm": "pass_q", "k_orth16": "orth", "k_qred16": "q_reduce",
-             "k_qred": "q_reduce", "k_qpad": "qpad", "k_qredl": "q_reduce", "k_qpadl": "qpad"}
+    fixed = {"k_pm": "pass_p", "k_qm": "pass_q", "k_qfin16": "q_finish", "k_qpad": "qpad",
+             "k_qredl": "q_reduce", "k_qpadl": "qpad"}
     if short in fixed:
         return fixed[short]
     if short == "k_mh16":

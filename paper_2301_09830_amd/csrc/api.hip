@@ -413,9 +413,10 @@ occ_status_t run_batch_t(const Batch& b, void* ws, uint32_t* flags, bool finish,
           if (b.descs[0].r != RP) L("qpad", k_qpad<RP>, b.blocks[K_QPAD]);
           for (int it = 0; it < b.iters; ++it) {
             LB("pass_p", k_pm<DT, VEC, RP, RM>, b.blocks[K_PASS_P], PM_THREADS);
-            LB("orth", k_orth16<RP>, b.blocks[K_PGRAM], CH_THREADS, flags);
-            LB("pass_q", k_qm<DT, VEC, RP, RM>, b.blocks[K_PASS_Q], QM_THREADS);
-            L("q_reduce", k_qred16<RP>, b.blocks[K_QRED]);
+            // T of each matrix (first `count` blocks) beside Q' = A^T P
+            LB("pass_q", k_qm<DT, VEC, RP, RM>, count + b.blocks[K_PASS_Q], QM_THREADS, flags);
+            L("q_finish", k_qfin16<RP>, b.blocks[K_QRED] + b.blocks[K_APPLY],
+              (int)b.blocks[K_QRED]);
           }
           if (finish) {
             if (write_mhat)

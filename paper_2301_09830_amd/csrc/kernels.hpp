@@ -121,15 +121,18 @@ __device__ __forceinline__ int find_matrix(const Desc* __restrict__ table, int c
   return lo;
 }
 
-// Dispatch helper: runs BODY(d, local_block) on the matrix owning this block.
-#define OCC_DISPATCH(KIND, BODY)                                        \
+// Dispatch helpers: run BODY(d, local_block) on the matrix owning block B
+// of kind KIND (this block, for OCC_DISPATCH).
+#define OCC_DISPATCH_AT(KIND, BODY, B)                                  \
   if (count == 1) {                                                     \
-    BODY(single, (int)blockIdx.x);                                      \
+    BODY(single, (B));                                                  \
   } else {                                                              \
-    const int j_ = find_matrix(table, count, KIND, (int)blockIdx.x);    \
+    const int j_ = find_matrix(table, count, KIND, (B));                \
     const Desc& d_ = table[j_];                                         \
-    BODY(d_, (int)blockIdx.x - d_.blk[KIND]);                           \
+    BODY(d_, (B) - d_.blk[KIND]);                                       \
   }
+
+#define OCC_DISPATCH(KIND, BODY) OCC_DISPATCH_AT(KIND, BODY, (int)blockIdx.x)
 
 #define OCC_KARGS const Desc* __restrict__ table, int count, Desc single
 

@@ -68,6 +68,15 @@ __device__ __forceinline__ f4v mfma4(float a, float b, f4v c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
+// v_mfma_f64_16x16x4_f64: the operands as in the fp32 form (lane (g, li)
+// supplies A[i = li][k = g] and B[k = g][j = li]), but component v of the
+// result holds D[i = 4 v + g][j = li] (rows interleaved across the four lane
+// groups; checked with an in-bounds probe on the MI355X).
+typedef double d4v __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ d4v mfma4d(double a, double b, d4v c) {
+  return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+}
+
 // Eight consecutive elements of A = M + err_prev (columns c..c+7 of one row),
 // kept as raw loads until used.  Out-of-range or unaligned chunks hold the
 // exact element-wise A in e0/e1 and -0 in m (x + -0 == x for every x).
@@ -415,16 +424,24 @@ __global__ __launch_bounds__(PM_THREADS) void k_pm(OCC_KARGS) {
 }
 
 // -------------------------------------------------------------------------
-// k_qm: right product partials on MFMA.  A block owns 128 columns and a row
-// split; each of its QM_WAVES waves takes a contiguous share of the split's
-// rows in 4-row K-steps.  The B operand is P_hat[row][li], read from the
-// P_hat buffer.  The waves' partial tiles are summed in LDS in wave order and
-// stored to qpart[split].
+// k_qm: right product partials on the fp64 matrix cores, Q' = A^T P on the
+// raw P (A^T P_hat = Q' T, with T applied by k_qfin16).  T cancels the
+// disparate scales and near-parallel directions of P's columns, so Q' is
+// accumulated in fp64 (A and P enter exactly): in fp32 the cancellation
+// amplified its rounding by up to the condition of P.  At rank 16 the fp64
+// products take about 14 us of matrix-core time on 8192 x 4096 against
+// about 25 us of memory time, so the pass stays memory-bound.
+//
+// A block owns 128 columns and a row split; each of its QM_WAVES waves takes
+// a contiguous share of the split's rows in 4-row K-steps.  The B operand is
+// P[row][li], read from the padded raw P.  The waves' partial tiles are
+// summed in LDS in a fixed order and stored (fp64) to qpart[split].  The
+// first `count` blocks of the grid instead form the orthogonalisation factor
+// T of one matrix each (orth_t_body): they are dispatched first and finish
+// while the streaming blocks run.
 // -------------------------------------------------------------------------
 struct QMSmem {
-  union {
-    float red[QM_WAVES * QM_COLS * 16];    // per-wave partial tiles
-  } u;
+  double red[QM_WAVES / 2][QM_COLS * 16];   // partial tiles of wave pairs (w, w + QM_WAVES / 2)
 };
 
 template <int DT, bool VEC, int RP, bool RM = false>
@@ -438,15 +455,15 @@ __device__ __forceinline__ void qm_body(const Desc& d, int b, QMSmem& sm) {
   const int nr = r_hi - r_lo;
   const int c0 = ct * QM_COLS;
 
-  const float* ps = p_src<RP>(d);
+  const float* ps = d.praw;
 
   const int wr = (nr + QM_WAVES - 1) / QM_WAVES;
   const int w_lo = r_lo + min(nr, wave * wr), w_hi = r_lo + min(nr, wave * wr + wr);
   const int nk = (w_hi - w_lo + 3) / 4;
   const int col = c0 + 8 * li;
-  f4v acc[8];
+  d4v acc[8];
 #pragma unroll
-  for (int t = 0; t < 8; ++t) acc[t] = f4v{0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < 8; ++t) acc[t] = d4v{0.0, 0.0, 0.0, 0.0};
   Ch8<DT> cur, nxt;
   float cp = 0.f, np = 0.f;
   {
@@ -465,37 +482,64 @@ __device__ __forceinline__ void qm_body(const Desc& d, int b, QMSmem& sm) {
     }
     float a[8];
     ch8_values<DT>(cur, a);
+    const double pd = (double)cp;
 #pragma unroll
-    for (int t = 0; t < 8; ++t) acc[t] = mfma4(a[t], cp, acc[t]);
+    for (int t = 0; t < 8; ++t) acc[t] = mfma4d((double)a[t], pd, acc[t]);
     if (more) {
       cur = nxt;
       cp = np;
     }
   }
 
-  // acc[t][v] = partial Q[c0 + 8(4g + v) + t][li] of this wave.
-  float* red = sm.u.red + wave * (QM_COLS * 16);
+  // acc[t][v] = partial Q'[c0 + 8(4v + g) + t][li] of this wave.  Waves
+  // w < QM_WAVES / 2 store theirs, waves w + QM_WAVES / 2 add theirs to
+  // them, and the pair sums are added in pair order.
+  constexpr int HW = QM_WAVES / 2;
+  double* red = sm.red[wave % HW];
+  if (wave < HW) {
 #pragma unroll
-  for (int t = 0; t < 8; ++t)
+    for (int t = 0; t < 8; ++t)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) red[(8 * (4 * g + v) + t) * 16 + li] = acc[t][v];
+      for (int v = 0; v < 4; ++v) red[(8 * (4 * v + g) + t) * 16 + li] = acc[t][v];
+  }
   __syncthreads();
+  if (wave >= HW) {
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int i = (8 * (4 * v + g) + t) * 16 + li;
+        red[i] = red[i] + acc[t][v];
+      }
+  }
+  __syncthreads();
+  double* qp = (double*)d.qpart;
   for (int e = threadIdx.x; e < QM_COLS * RP; e += QM_THREADS) {
     const int cl = e / RP, k = e % RP;
     const int gcol = c0 + cl;
     if (gcol >= d.n) continue;
-    float v = sm.u.red[cl * 16 + k];
+    double v = sm.red[0][cl * 16 + k];
 #pragma unroll
-    for (int w = 1; w < QM_WAVES; ++w) v = v + sm.u.red[w * QM_COLS * 16 + cl * 16 + k];
-    d.qpart[((int64_t)s * d.n + gcol) * RP + k] = v;
+    for (int w = 1; w < HW; ++w) v = v + sm.red[w][cl * 16 + k];
+    qp[((int64_t)s * d.n + gcol) * RP + k] = v;
   }
 }
 
+union QMOSmem {
+  QMSmem q;
+  CholSmem c;
+};
+
 template <int DT, bool VEC, int RP, bool RM = false>
-__global__ __launch_bounds__(QM_THREADS) void k_qm(OCC_KARGS) {
-  __shared__ __attribute__((aligned(16))) QMSmem sm;
-#define B_(d, b) qm_body<DT, VEC, RP, RM>(d, b, sm)
-  OCC_DISPATCH(K_PASS_Q, B_)
+__global__ __launch_bounds__(QM_THREADS) void k_qm(OCC_KARGS, uint32_t* flags) {
+  __shared__ __attribute__((aligned(16))) QMOSmem sm;
+  const int b = (int)blockIdx.x;
+  if (b < count) {
+    orth_t_body<RP, QM_THREADS>(count == 1 ? single : table[b], flags, sm.c);
+    return;
+  }
+#define B_(d, bb) qm_body<DT, VEC, RP, RM>(d, bb, sm.q)
+  OCC_DISPATCH_AT(K_PASS_Q, B_, b - count)
 #undef B_
 }
 

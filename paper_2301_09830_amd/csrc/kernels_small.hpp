@@ -106,15 +106,18 @@ __device__ __forceinline__ void gram_rows_store(const double* rows, int nr, doub
 }
 
 // -------------------------------------------------------------------------
-// k_orth16: Gram = sum of the row-block partials, Cholesky G = R^T R
-// (CholeskyQR first pass) and, only when the first pass lost orthogonality,
-// the second pass; then P_hat = P R^-1 by forward substitution, one row per
-// thread.  Blocks of 1024 threads: thread (pair, group) sums a slice of the
-// packed partials with all its loads in flight, the slices are added in LDS
-// in order, and wave 0 factorises with one matrix entry per lane slot.
+// Orthogonalisation of the small-rank path (Sec. 2.3 CholeskyQR; the second
+// pass only when the first lost orthogonality).  P_hat = P T with
+// T = R1^-1 (R2^-1), so A^T P_hat = (A^T P) T: the right product runs on the
+// raw P, and T is formed by one block per matrix that runs beside it (the
+// first blocks of k_qm): Gram = sum of the row-block partials (slice
+// (entry, group) per thread pair, loads in flight, slices added in LDS in
+// order), Cholesky by wave 0 with one matrix entry per lane slot, T stored
+// to d.t1.  k_qfin16 then applies T to the summed right-product partials
+// and to P.  The chain Gram -> Cholesky -> T thus overlaps the streaming
+// pass instead of running between the two products.
 // -------------------------------------------------------------------------
-constexpr int CH_THREADS = 1024;
-static_assert(F_ORTHROWS <= CH_THREADS, "k_orth16 forms one P_hat row per thread");
+constexpr int CH_SLICES_MAX = 1024;  // thread pairs the Gram sum is sliced for (fixes its order)
 constexpr int CH_CHUNK = 256;     // rows per chunk of the second-pass Gram
 constexpr int CH_BATCH = 20;      // partial loads in flight per thread
 
@@ -247,15 +250,18 @@ __device__ __forceinline__ void solve_row(double* x, const double* R, const doub
   }
 }
 
-// Gram (upper triangle, fp64) of `nsrc` stacked packed partials, by all
-// CH_THREADS threads; result (full symmetric) in G.
-template <int RP>
+// Gram (upper triangle, fp64) of `nsrc` stacked packed partials, by NT
+// threads; result (full symmetric) in G.  The partials are cut into NG
+// consecutive slices, each summed in order, and the slices are added in
+// order (NG depends on the rank only, so the sum does not depend on NT).
+template <int RP, int NT>
 __device__ __forceinline__ void gram_sum_all(const double* src, int nsrc, CholSmem& sm, double* G) {
   constexpr int NP = RP * (RP + 1) / 2;
-  constexpr int NG = CH_THREADS / NP < 8 ? CH_THREADS / NP : 8;
+  constexpr int NG = CH_SLICES_MAX / NP < 8 ? CH_SLICES_MAX / NP : 8;
+  static_assert(NP <= NT, "one thread per entry for the slice sum");
   const int t = threadIdx.x;
-  const int p = t % NP, q = t / NP;
-  if (q < NG) {
+  for (int pr = t; pr < NG * NP; pr += NT) {
+    const int p = pr % NP, q = pr / NP;
     const int per = (nsrc + NG - 1) / NG;
     const int g0 = min(nsrc, q * per), g1 = min(nsrc, g0 + per);
     double s = 0.0;
@@ -291,21 +297,17 @@ __device__ __forceinline__ void p_row(const Desc& d, int64_t row, double* x) {
   }
 }
 
-// k_orth16 block b: full Gram, Cholesky (and the second pass when needed),
-// computed identically in every block, then P_hat = P T for the rows of its
-// 128-row chunks (one chunk per block up to 64 blocks, consecutive chunks
-// beyond), written to the caller's P and the padded copy.  Block 0 also stores the second-pass decision and the
-// numeric flags.
-template <int RP>
-__device__ __forceinline__ void orth16_body(const Desc& d, int b, uint32_t* flags, CholSmem& sm) {
+// T of one matrix by one block of NT threads (see above); also stores the
+// second-pass decision (d.info[0]) and the numeric flags.
+template <int RP, int NT>
+__device__ __forceinline__ void orth_t_body(const Desc& d, uint32_t* flags, CholSmem& sm) {
   const int t = threadIdx.x;
-  uint32_t* fl = (b == 0) ? flags : nullptr;
-  gram_sum_all<RP>(d.gpart, d.ng, sm, sm.G);
+  gram_sum_all<RP, NT>(d.gpart, d.ng, sm, sm.G);
   if (t < kWave) {
-    const CholInfo o = chol_lanes<RP>(sm.G, d.r, sm.R[0], sm.inv[0], fl);
+    const CholInfo o = chol_lanes<RP>(sm.G, d.r, sm.R[0], sm.inv[0], flags);
     const uint32_t need = needs_second_pass(o);
     if (t == 0) {
-      if (b == 0) d.info[0] = need;
+      d.info[0] = need;
       sm.need = need;
     }
   }
@@ -314,7 +316,8 @@ __device__ __forceinline__ void orth16_body(const Desc& d, int b, uint32_t* flag
   if (need) {
     // Second pass: Gram of P_hat1 = P R1^-1 (fp64) over all rows, in chunks.
     constexpr int NP = RP * (RP + 1) / 2;
-    constexpr int NG = CH_THREADS / NP < 8 ? CH_THREADS / NP : 8;
+    constexpr int NG = NT / NP < 8 ? NT / NP : 8;
+    static_assert(CH_CHUNK <= NT, "one row of a chunk per thread");
     const int p = t % NP, q = t / NP;
     int pk_, pl_;
     upper_entry<RP>(p, pk_, pl_);
@@ -349,14 +352,12 @@ __device__ __forceinline__ void orth16_body(const Desc& d, int b, uint32_t* flag
       sm.G[pl_ * RP + pk_] = sacc;
     }
     __syncthreads();
-    if (t < kWave) chol_lanes<RP>(sm.G, d.r, sm.R[1], sm.inv[1], fl);
+    if (t < kWave) chol_lanes<RP>(sm.G, d.r, sm.R[1], sm.inv[1], flags);
     __syncthreads();
   }
   // The substitution x -> x R1^-1 (R2^-1) is linear, so P_hat = P T with row
   // i of T the image of the unit row e_i (upper triangular; a dependent
-  // column's inverse diagonal is zero, so its column of T is zero): RP
-  // threads form T in fp64, then every row of P_hat is a product with T,
-  // TPR threads per row each forming OPT of its columns.
+  // column's inverse diagonal is zero, so its column of T is zero).
   if (t < RP) {
     double x[RP];
 #pragma unroll
@@ -364,82 +365,88 @@ __device__ __forceinline__ void orth16_body(const Desc& d, int b, uint32_t* flag
     solve_row<RP>(x, sm.R[0], sm.inv[0]);
     if (need) solve_row<RP>(x, sm.R[1], sm.inv[1]);
 #pragma unroll
-    for (int k = 0; k < RP; ++k) sm.T[t * RP + k] = x[k];
+    for (int k = 0; k < RP; ++k) d.t1[t * RP + k] = x[k];
   }
-  __syncthreads();
-  constexpr int OPT = RP >= 16 ? RP / 8 : 1;   // columns of P_hat per thread
-  constexpr int TPR = RP / OPT;                // threads per row
-  static_assert(F_ORTHROWS * TPR <= CH_THREADS, "a chunk's rows at once");
-  const int i = t / TPR, j0 = (t % TPR) * OPT;
-  double tc[OPT][RP];   // this thread's columns of T
+}
+
+// -------------------------------------------------------------------------
+// k_qfin16: the factor T applied.  Blocks [0, nq) (kind K_QRED): for
+// kBlock / RP columns c each, Q'[c][k] = sum over row splits of the fp64
+// qpart[s][c][k] (in split order), then Q[c][j] = sum_k Q'[c][k] T[k][j]
+// (fp64, k ascending), written to the caller's Q and the padded copy.
+// Blocks [nq, ...) (kind K_APPLY): for kBlock / RP rows each,
+// P_hat[i][j] = sum_k P[i][k] T[k][j] (fp64, k ascending), written to the
+// caller's P and the padded copy.
+// -------------------------------------------------------------------------
+template <int RP>
+__device__ __forceinline__ void load_t(const Desc& d, double* Ts) {
+  for (int e = threadIdx.x; e < RP * RP; e += kBlock) Ts[e] = d.t1[e];
+}
+
+template <int RP>
+__device__ __forceinline__ void qfin_q_body(const Desc& d, int b, double* Ts, double* qs) {
+  constexpr int CPB = kBlock / RP;
+  const int t = threadIdx.x, cl = t / RP, k = t % RP;
+  load_t<RP>(d, Ts);
+  const double* qp = (const double*)d.qpart;
+  const int64_t c = (int64_t)b * CPB + cl;
+  const int64_t idx = c * RP + k;
+  double acc = 0.0;
+  if (c < d.n) {
+    for (int t0 = 0; t0 < d.sq; t0 += 16) {
+      double v[16];
 #pragma unroll
-  for (int q = 0; q < OPT; ++q)
+      for (int u = 0; u < 16; ++u) v[u] = (t0 + u < d.sq) ? qp[(int64_t)(t0 + u) * d.n * RP + idx] : 0.0;
 #pragma unroll
-    for (int k = 0; k < RP; ++k) tc[q][k] = sm.T[k * RP + j0 + q];
-  // this block's 128-row chunks: [b per, (b + 1) per) of the nch chunks
-  const int nch = (d.m + F_ORTHROWS - 1) / F_ORTHROWS;
-  const int per = (nch + orth_blocks(d.m) - 1) / orth_blocks(d.m);
-  for (int c = b * per; c < min(nch, (b + 1) * per); ++c) {
-    const int64_t row = (int64_t)c * F_ORTHROWS + i;
-    if (i < F_ORTHROWS && row < d.m) {
-      double x[RP];
-      p_row<RP>(d, row, x);
-      float out[OPT];
-#pragma unroll
-      for (int q = 0; q < OPT; ++q) {
-        double acc = 0.0;
-#pragma unroll
-        for (int k = 0; k < RP; ++k) acc = fma(x[k], tc[q][k], acc);
-        out[q] = (float)acc;
-      }
-      // the padded copy is always written: the reconstruction pass reads it
-      // with 16-byte loads (the caller's P has no alignment guarantee)
-      if constexpr (OPT == 2)
-        *(float2*)(d.phat + row * RP + j0) = make_float2(out[0], out[1]);
-      else
-        d.phat[row * RP + j0] = out[0];
-#pragma unroll
-      for (int q = 0; q < OPT; ++q)
-        if (j0 + q < d.r) d.P[row * d.r + j0 + q] = out[q];
+      for (int u = 0; u < 16; ++u)
+        if (t0 + u < d.sq) acc = (t0 + u == 0) ? v[u] : acc + v[u];
     }
   }
+  qs[t] = acc;
+  __syncthreads();
+  if (c >= d.n) return;
+  double q = 0.0;
+#pragma unroll
+  for (int kk = 0; kk < RP; ++kk) q = fma(qs[cl * RP + kk], Ts[kk * RP + k], q);
+  const float v = (float)q;
+  d.qpad[idx] = v;   // always: the next left product and the reconstruction read the padded copy
+  if (k < d.r) d.Q[c * d.r + k] = v;
 }
 
 template <int RP>
-__global__ __launch_bounds__(CH_THREADS) void k_orth16(OCC_KARGS, uint32_t* flags) {
-  __shared__ CholSmem sm;
-#define B_(d, b) orth16_body<RP>(d, b, flags, sm)
-  OCC_DISPATCH(K_PGRAM, B_)
+__device__ __forceinline__ void qfin_p_body(const Desc& d, int b, double* Ts) {
+  constexpr int RPB = kBlock / RP;
+  const int t = threadIdx.x, j = t % RP;
+  load_t<RP>(d, Ts);
+  __syncthreads();
+  const int64_t row = (int64_t)b * RPB + t / RP;
+  if (row >= d.m) return;
+  double x[RP];
+  p_row<RP>(d, row, x);
+  double acc = 0.0;
+#pragma unroll
+  for (int k = 0; k < RP; ++k) acc = fma(x[k], Ts[k * RP + j], acc);
+  const float out = (float)acc;
+  // the padded copy is always written: the reconstruction pass reads it
+  // with 16-byte loads (the caller's P has no alignment guarantee)
+  d.phat[row * RP + j] = out;
+  if (j < d.r) d.P[row * d.r + j] = out;
+}
+
+template <int RP>
+__global__ __launch_bounds__(kBlock) void k_qfin16(OCC_KARGS, int nq) {
+  __shared__ double Ts[RP * RP];
+  __shared__ double qs[kBlock];
+  const int b = (int)blockIdx.x;
+  if (b < nq) {
+#define B_(d, bb) qfin_q_body<RP>(d, bb, Ts, qs)
+    OCC_DISPATCH_AT(K_QRED, B_, b)
 #undef B_
-}
-
-// -------------------------------------------------------------------------
-// k_qred16: Q[c][k] = sum over row splits of qpart[s][c][k] (fixed order),
-// written to the caller's Q and the padded copy.
-// -------------------------------------------------------------------------
-template <int RP>
-__device__ __forceinline__ void qred16_body(const Desc& d, int b) {
-  const int64_t idx = (int64_t)b * kBlock + threadIdx.x;
-  if (idx >= (int64_t)d.n * RP) return;
-  const int c = (int)(idx / RP), k = (int)(idx % RP);
-  float acc = 0.f;
-  for (int t0 = 0; t0 < d.sq; t0 += 8) {
-    float v[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = (t0 + u < d.sq) ? d.qpart[(int64_t)(t0 + u) * d.n * RP + idx] : 0.f;
-#pragma unroll
-    for (int u = 0; u < 8; ++u)
-      if (t0 + u < d.sq) acc = (t0 + u == 0) ? v[u] : acc + v[u];
+  } else {
+#define B_(d, bb) qfin_p_body<RP>(d, bb, Ts)
+    OCC_DISPATCH_AT(K_APPLY, B_, b - nq)
+#undef B_
   }
-  d.qpad[idx] = acc;   // always: the reconstruction pass reads the padded copy
-  if (k < d.r) d.Q[(int64_t)c * d.r + k] = acc;
-}
-
-template <int RP>
-__global__ __launch_bounds__(kBlock) void k_qred16(OCC_KARGS) {
-#define B_(d, b) qred16_body<RP>(d, b)
-  OCC_DISPATCH(K_QRED, B_)
-#undef B_
 }
 
 }  // namespace occ

@@ -45,7 +45,7 @@ struct Desc {
   float* phat;           // m x rp
   float* praw;           // m x rp
   float* ppart;          // sp x m x rp
-  float* qpart;          // sq x n x rp
+  float* qpart;          // sq x n x rp (fp64 on the small-rank path)
   double* gpart;         // ng x rp x rp
   double* gsum;          // rp x rp
   double* t1;            // rp x rp
@@ -99,17 +99,7 @@ constexpr int F_QCOLS = 128;      // right product: columns per block
 constexpr int F_MHCOLS = 128;     // reconstruction: columns per block
 constexpr int F_MHGROUP = 64;     // reconstruction: rows per block step (4 waves x 16 rows)
 constexpr int F_MHBLOCKS = 1024;  // reconstruction: target number of blocks
-constexpr int F_QBLOCKS = 512;    // right product: target number of blocks
-constexpr int F_ORTHROWS = 128;   // Cholesky/P_hat kernel: rows of P_hat per chunk
-// Cholesky/P_hat kernel: blocks per matrix, at most.  Every block sums all
-// Gram partials (and, for a second CholeskyQR pass, forms the second Gram over
-// all rows), so the block count is capped to keep that work linear in m; a
-// block then forms P_hat for several consecutive 128-row chunks.
-constexpr int F_ORTHBLOCKS = 64;
-__host__ __device__ inline int orth_blocks(int64_t m) {
-  const int64_t chunks = (m + F_ORTHROWS - 1) / F_ORTHROWS;
-  return (int)(chunks < F_ORTHBLOCKS ? chunks : F_ORTHBLOCKS);
-}
+constexpr int F_QBLOCKS = 512;    // right product: resident blocks (2 per CU on 256 CUs)
 
 // Large-rank path (padded rank 32, 64, 128): tile constants shared with
 // kernels_large.hpp.
@@ -156,8 +146,10 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0,
     t.sp = 1;
     t.p_cols = (int)round_up(n, 32);
     t.ng = (int)p_blocks;
+    // right product: at most F_QBLOCKS - 1 blocks, so that they and the
+    // block forming T run in one round
     const int64_t col_tiles = cdiv(n, F_QCOLS);
-    const int64_t sq = clamp64(cdiv(F_QBLOCKS, col_tiles), 1, cdiv(m, 32));
+    const int64_t sq = clamp64((F_QBLOCKS - 1) / col_tiles, 1, cdiv(m, 32));
     t.q_rows = (int)round_up(cdiv(m, sq), 4);
     t.sq = (int)cdiv(m, t.q_rows);
     // reconstruction: 128-column tiles x row blocks (multiple of 64 rows),
@@ -167,9 +159,9 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0,
     t.mr = (int)round_up(cdiv(m, rbm), F_MHGROUP);
     t.blocks[K_QPAD] = cdiv((int64_t)t.n_pad * rp, kBlock);
     t.blocks[K_PASS_P] = p_blocks;
-    t.blocks[K_PGRAM] = orth_blocks(m);
-    t.blocks[K_PASS_Q] = col_tiles * t.sq;
+    t.blocks[K_PASS_Q] = col_tiles * t.sq;   // plus one block per matrix forming T
     t.blocks[K_QRED] = cdiv(n * rp, kBlock);
+    t.blocks[K_APPLY] = cdiv(m * rp, kBlock);
     t.blocks[K_MHAT] = ctm * cdiv(m, t.mr);
     return t;
   }
@@ -255,7 +247,7 @@ inline Regions matrix_regions(int64_t m, int64_t n, int rp, const Tiling& t) {
   g.phat = take((size_t)m * rp * 4);
   g.praw = take((size_t)m * rp * 4);
   g.ppart = take((size_t)t.sp * m * rp * 4);
-  g.qpart = take((size_t)t.sq * n * rp * 4);
+  g.qpart = take((size_t)t.sq * n * rp * (rp <= kFusedMaxRank ? 8 : 4));   // fp64 at rank <= 16
   g.gpart = take((size_t)t.ng * rp * rp * 8);
   g.gsum = take((size_t)rp * rp * 8);
   g.t1 = take((size_t)rp * rp * 8);
