@@ -45,13 +45,25 @@ PROFILES = os.path.join(ROOT, "profiles")
 CSRC = os.path.join(ROOT, "paper_2301_09830_amd", "csrc")
 
 
+def code_lines(text: str) -> str:
+    """C++ source without its line comments, trailing blanks and empty lines
+    (the library's sources hold no "//" inside string literals)."""
+    out = []
+    for line in text.splitlines():
+        line = line.split("//", 1)[0].rstrip()
+        if line:
+            out.append(line)
+    return "\n".join(out)
+
+
 def kernel_source_digest() -> str:
-    """Digest of the library sources; counter summaries apply only to it."""
+    """Digest of the library's code (comments excluded); counter summaries
+    apply only to it."""
     h = hashlib.sha256()
     for path in sorted(glob.glob(os.path.join(CSRC, "*.hpp")) + glob.glob(os.path.join(CSRC, "*.hip"))):
-        with open(path, "rb") as f:
+        with open(path, encoding="utf-8") as f:
             h.update(os.path.basename(path).encode())
-            h.update(f.read())
+            h.update(code_lines(f.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -1,20 +1,20 @@
 // Fused small-rank path of liboptcc (padded rank RP <= 16): helpers, the
-// Cholesky, P_hat and Q-reduction kernels and the reconstruction pass.
+// orthogonalisation factor, the finishing kernel and the reconstruction pass.
 //
-// One power-iteration round is four launches; kernel boundaries are the only
-// device-wide synchronisation on the streaming passes (an agent-scope
-// release fence in every block of a streaming kernel writes back the XCD's
-// L2 and costs more than a launch):
+// One power-iteration round is three launches; kernel boundaries are the
+// only device-wide synchronisation (an agent-scope release fence in every
+// block of a streaming kernel writes back the XCD's L2 and costs more than a
+// launch):
 //   k_pm     left product P = A Q on the matrix cores (kernels_mfma16.hpp);
 //            each block owns whole rows, so it stores final rows of P and
 //            their fp64 Gram partial.
-//   k_orth16 every block sums the Gram partials and runs the Cholesky
-//            factorisation G = R^T R (CholeskyQR first pass; the second pass
-//            only when the first found the Gram badly conditioned) -- the
-//            same deterministic computation in each block, so no hand-off is
-//            needed -- then forms P_hat = P R^-1 for its own 128 rows.
-//   k_qm     right product partials A^T P_hat over row splits (matrix cores).
-//   k_qred16 Q = sum of the row-split partials.
+//   k_qm     right product partials Q' = A^T P on the raw P over row splits
+//            (fp64 matrix cores, kernels_mfma16.hpp); its first block per
+//            matrix sums the Gram partials, runs the Cholesky G = R^T R
+//            (CholeskyQR first pass; the second only when the first found the
+//            Gram badly conditioned) and stores T = R^-1, so that P_hat = P T
+//            and A^T P_hat = Q' T.
+//   k_qfin16 Q = (sum of the split partials) T and P_hat = P T.
 // and after the last round
 //   k_mh16   reconstruction and residual, M_hat = P_hat Q^T and
 //            err = A - M_hat (matrix cores, kernels_mfma16.hpp).
