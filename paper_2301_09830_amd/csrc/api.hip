@@ -181,7 +181,8 @@ Slots device_slots_for(int dev) {
   constexpr bool X3 = DT == DT_BF16;
   int bp = 0, bq = 0, bm = 0;
   bool ok = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-                 &bp, k_lp<DT, RP, SA_MERR_SAVE, X3, true>, kBlock, 0) == hipSuccess;
+                 &bp, k_lp<DT, RP, SA_MERR_SAVE, X3, true>, lp_block_rows(RP, X3) / 32 * kWave,
+                 0) == hipSuccess;
   if constexpr (X3)
     ok = ok && hipOccupancyMaxActiveBlocksPerMultiprocessor(&bq, k_lqx<DT_F32, RP, SA_SAVED, true>,
                                                             kBlock, 0) == hipSuccess;
@@ -282,7 +283,8 @@ occ_status_t plan_batch(const occ_mat_t* mats, int count, int rank, int iters, u
   for (int j = 0; j < count; ++j) {
     const occ_mat_t& a = mats[j];
     const Tiling t =
-        make_tiling(a.rows, a.cols, b.rp, (double)a.rows * (double)a.cols / total_elems, slots);
+        make_tiling(a.rows, a.cols, b.rp, (double)a.rows * (double)a.cols / total_elems, slots,
+                    dt == OCC_BF16);
     const Regions g = matrix_regions(a.rows, a.cols, b.rp, t);
     Desc& d = b.descs[j];
     d.m = (int32_t)a.rows;
@@ -440,6 +442,7 @@ occ_status_t run_batch_t(const Batch& b, void* ws, uint32_t* flags, bool finish,
         // and the reconstruction (err and M_hat rows) use it: the stored A is
         // compact, so every pass in between is the dense kernel.
         constexpr bool TL = true;
+        constexpr int LPT = lp_block_rows(RP, X3) / 32 * kWave;   // threads of a left-product block
         bool whole = VEC;
         for (const Desc& dd : b.descs) whole = whole && dd.n % 32 == 0;
         const bool tiles_merr = whole && b.descs[0].err_in != nullptr;
@@ -447,19 +450,19 @@ occ_status_t run_batch_t(const Batch& b, void* ws, uint32_t* flags, bool finish,
         for (int it = 0; it < b.iters; ++it) {
           if (!saved) {
             if (tiles_merr)
-              L("pass_p", k_lp<DT, RP, SA_MERR, X3, TL, RM>, b.blocks[K_PASS_P]);
+              LB("pass_p", k_lp<DT, RP, SA_MERR, X3, TL, RM>, b.blocks[K_PASS_P], LPT);
             else
-              L("pass_p", k_lp<DT, RP, SA_MERR, X3, false, RM>, b.blocks[K_PASS_P]);
+              LB("pass_p", k_lp<DT, RP, SA_MERR, X3, false, RM>, b.blocks[K_PASS_P], LPT);
           } else if (it == 0) {
             if (tiles_merr)
-              L("pass_p_first", k_lp<DT, RP, SA_MERR_SAVE, X3, TL, RM>, b.blocks[K_PASS_P]);
+              LB("pass_p_first", k_lp<DT, RP, SA_MERR_SAVE, X3, TL, RM>, b.blocks[K_PASS_P], LPT);
             else
-              L("pass_p_first", k_lp<DT, RP, SA_MERR_SAVE, X3, false, RM>, b.blocks[K_PASS_P]);
+              LB("pass_p_first", k_lp<DT, RP, SA_MERR_SAVE, X3, false, RM>, b.blocks[K_PASS_P], LPT);
           } else {
             if (whole)
-              L("pass_p_a", k_lp<DT_F32, RP, SA_SAVED, X3, TL>, b.blocks[K_PASS_P]);
+              LB("pass_p_a", k_lp<DT_F32, RP, SA_SAVED, X3, TL>, b.blocks[K_PASS_P], LPT);
             else
-              L("pass_p_a", k_lp<DT_F32, RP, SA_SAVED, X3, false>, b.blocks[K_PASS_P]);
+              LB("pass_p_a", k_lp<DT_F32, RP, SA_SAVED, X3, false>, b.blocks[K_PASS_P], LPT);
           }
           L("gram", k_lg<RP, 0>, b.blocks[K_PGRAM]);
           L("gram_sum", k_gsum<RP, 0>, b.blocks[K_GSUM]);

@@ -199,7 +199,8 @@ __device__ __forceinline__ int kcol_of(int c_lo, int ks0, int it, int nk) {
 }
 
 // -------------------------------------------------------------------------
-// k_lp: P partials = A Q for one 128-row tile and one column split.
+// k_lp: P partials = A Q for one row tile (lp_block_rows: 32 rows per wave)
+// and one column split.
 //
 // X3 (bf16 M): the products run on v_mfma_f32_32x32x16_bf16 with each
 // operand split in two bf16 parts, x = x_hi + x_lo (x - x_hi - x_lo is below
@@ -399,16 +400,18 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b,
                                         uint8_t* tiles) {
   constexpr int NU = RP / 32;               // rank tiles
   constexpr int QP = RP + 4;                // LDS pitch of a Q row (fp32 form)
+  constexpr int LR = lp_block_rows(RP, X3);  // rows per block, 32 per wave
+  constexpr int NT = LR / 32 * kWave;        // threads per block
   // 16-byte chunks of one K-step's Q tile per thread: fp32 form RP x 32 x 4 B,
   // bf16 form 2 x RP x 32 x 2 B (the same count)
-  constexpr int QF4 = L_KC * RP / 4 / kBlock;
-  static_assert(QF4 * 4 * kBlock == L_KC * RP, "Q tile must split evenly");
+  constexpr int QF4 = L_KC * RP / 4 / NT;
+  static_assert(QF4 * 4 * NT == L_KC * RP, "Q tile must split evenly");
   const bool vec = d.vec != 0;
   const int wave = wave_id(), lane = threadIdx.x & 63;
   const int li = lane & 31, g = lane >> 5;
-  const int row_tiles = (d.m + L_PROWS - 1) / L_PROWS;
+  const int row_tiles = (d.m + LR - 1) / LR;
   const int rt = b % row_tiles, s = b / row_tiles;
-  const int row = rt * L_PROWS + 32 * wave + li;
+  const int row = rt * LR + 32 * wave + li;
   const int c_lo = s * d.p_cols;
   const int c_hi = min(d.n, c_lo + d.p_cols);
   const int nk = (c_hi - c_lo + L_KC - 1) / L_KC;
@@ -425,7 +428,7 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b,
   // tile is in bounds (rows past n are zero); bf16 form: qbf rows have n_pad
   // columns, likewise zero past n.
   auto q_src_ptr = [&](int c, int x) -> const f4v* {
-    const int f = threadIdx.x + kBlock * x;
+    const int f = threadIdx.x + NT * x;
     if constexpr (X3) {
       const int h = f / (RP * 4), rem = f % (RP * 4);
       return (const f4v*)(d.qbf + ((int64_t)h * RP + rem / 4) * d.n_pad + c + 8 * (rem % 4));
@@ -434,7 +437,7 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b,
     }
   };
   auto q_lds_ptr = [&](int stage, int x) -> f4v* {
-    const int f = threadIdx.x + kBlock * x;
+    const int f = threadIdx.x + NT * x;
     if constexpr (X3) {
       const int h = f / (RP * 4), rem = f % (RP * 4);
       return (f4v*)(&sm.q[stage][h][(rem / 4) * LB_P + 8 * (rem % 4)]);
@@ -511,7 +514,7 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b,
   if constexpr (TILES) {
     constexpr int SB = LPTile<DT, SA>::BYTES;
     uint8_t* const wt = tiles + wave * 2 * SB;   // this wave's two stages
-    const int wrow0 = rt * L_PROWS + 32 * wave;
+    const int wrow0 = rt * LR + 32 * wave;
     const LPRows prw = lp_rows<DT, RM && SA != SA_SAVED>(d, wrow0);
     lp_tile_issue<DT, SA, RM>(d, wrow0, kcol_of(c_lo, ks0, 0, nk), wt, prw);
     __syncthreads();
@@ -561,11 +564,11 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b,
     }
   }
 
-  // acc[u][v] = P[rt*128 + 32*wave + mf32_row(v, g)][NU*li + u] (this split)
+  // acc[u][v] = P[rt*LR + 32*wave + mf32_row(v, g)][NU*li + u] (this split)
   float* dst = d.ppart + (int64_t)s * d.m * RP;
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
-    const int r = rt * L_PROWS + 32 * wave + mf32_row(v, g);
+    const int r = rt * LR + 32 * wave + mf32_row(v, g);
     if (r < d.m) {
       float o[NU];
 #pragma unroll
@@ -576,9 +579,10 @@ __device__ __forceinline__ void lp_body(const Desc& d, int b,
 }
 
 template <int DT, int RP, int SA, bool X3, bool TILES, bool RM = false>
-__global__ __launch_bounds__(kBlock) void k_lp(OCC_KARGS) {
+__global__ __launch_bounds__(lp_block_rows(RP, X3) / 32 * kWave) void k_lp(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) std::conditional_t<X3, LPXSmem<RP>, LPSmem<RP>> sm;
-  __shared__ __attribute__((aligned(16))) uint8_t tiles[TILES ? 4 * 2 * LPTile<DT, SA>::BYTES : 16];
+  __shared__ __attribute__((aligned(16))) uint8_t
+      tiles[TILES ? lp_block_rows(RP, X3) / 32 * 2 * LPTile<DT, SA>::BYTES : 16];
 #define B_(d, b) lp_body<DT, RP, SA, X3, TILES, RM>(d, b, sm, tiles)
   OCC_DISPATCH(K_PASS_P, B_)
 #undef B_

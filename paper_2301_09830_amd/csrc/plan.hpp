@@ -103,7 +103,11 @@ constexpr int F_QBLOCKS = 512;    // right product: resident blocks (2 per CU on
 
 // Large-rank path (padded rank 32, 64, 128): tile constants shared with
 // kernels_large.hpp.
-constexpr int L_PROWS = 128;      // left product: rows per block (4 waves x 32)
+constexpr int L_PROWS = 128;      // left product: rows per block (4 waves x 32) ...
+// ... and 256 (8 waves) for bf16 M at padded rank 128, where a 4-wave block
+// runs one wave per SIMD (its LDS tiles and Q stages) and reads a Q tile as
+// large as its A tile
+__host__ __device__ constexpr int lp_block_rows(int rp, bool x3) { return rp >= 128 && x3 ? 256 : L_PROWS; }
 constexpr int L_KC = 32;          // left product: columns per K-step
 constexpr int L_GROWS = 256;      // Gram partials: rows per block
 constexpr int L_AROWS = 128;      // P_hat = P T: rows per block
@@ -136,7 +140,7 @@ inline int64_t whole_rounds(int64_t want, int64_t slots) {
 // share: this matrix's fraction of the elements of the whole call (the
 // large-rank grids are sized for the batch).
 inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0,
-                          const Slots& sl = Slots{}) {
+                          const Slots& sl = Slots{}, bool x3 = false) {
   Tiling t{};
   t.n_pad = (int)round_up(n, 32);
   t.m_pad = (int)round_up(m, 32);
@@ -184,7 +188,7 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0,
   // wide -- narrower, down to L_MIN_NARROW, while this matrix's blocks would
   // leave its share of one round of resident blocks partly empty (a matrix of
   // few rows, e.g. the rows of a row-sparse step)
-  const int64_t row_tiles = cdiv(m, L_PROWS);
+  const int64_t row_tiles = cdiv(m, lp_block_rows(rp, x3));
   int64_t min_cols = L_MIN_COLS;
   auto sp_of = [&](int64_t mc) { return clamp64(cdiv(target, row_tiles), 1, cdiv(n, mc)); };
   while (min_cols > L_MIN_NARROW && row_tiles * sp_of(min_cols) < (int64_t)(share * (double)sl.p))
