@@ -50,6 +50,18 @@ def test_rank_sweep_fp32(rank, iters):
     assert_parity(res, "f32", f"sweep 300x257 r{rank} t{iters}")
 
 
+@pytest.mark.parametrize("rank", [4, 16, 32])
+def test_max_iterations(rank):
+    """OCC_MAX_ITERS (64) power-iteration rounds per step on a low-rank matrix
+    whose spectrum (1/j, j = 1..48, noise 1e-4) separates every leading
+    subspace used here: the rounds contract towards it, so the fp32 and
+    float64 trajectories stay together through all 64."""
+    w = Workload(91, "maxiter", ((300, 257),), "f32", rank, 64, 2, "lowrank",
+                 signal_rank=48, noise=1e-4)
+    res, _, _ = run_workload(w, 2)
+    assert_parity(res, "f32", f"lowrank 300x257 r{rank} t64")
+
+
 @pytest.mark.parametrize("rank", [4, 16, 33, 128])
 def test_rank_sweep_bf16(rank):
     w = WORKLOADS[2].scaled([(600, 333)], rank=rank, signal_rank=48)
