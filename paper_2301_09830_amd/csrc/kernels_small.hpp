@@ -74,12 +74,10 @@ __device__ __forceinline__ void chunk_value(const AChunk<DT>& x, float a[4]) {
   }
 }
 
-// Source of the factors: the caller's P/Q when rank == RP (same layout),
-// else the padded workspace copies.
+// Source of the warm-start or previous round's Q: the caller's Q when
+// rank == RP (same layout), else the padded workspace copy.
 template <int RP>
 __device__ __forceinline__ const float* q_src(const Desc& d) { return d.r == RP ? d.Q : d.qpad; }
-template <int RP>
-__device__ __forceinline__ const float* p_src(const Desc& d) { return d.r == RP ? d.P : d.phat; }
 
 // Packed upper triangle of an RP x RP symmetric matrix: entry p < NP
 // (NP = RP (RP + 1) / 2) is (k, l) with k <= l, row by row.
