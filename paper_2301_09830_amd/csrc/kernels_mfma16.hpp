@@ -1,12 +1,13 @@
 // Small-rank products on the matrix cores (padded rank RP <= 16).
 //
 // Both tall-skinny products of a power-iteration round are dense
-// contractions with a 16-wide output dimension; v_mfma_f32_16x16x4_f32 takes
-// its two operands spread over the 64 lanes (one value per lane), so the
-// 16-wide factor (Q rows in the left product, P_hat rows in the right one)
-// never has to be broadcast, and A goes straight from 16-byte global loads
-// into the instruction.  Arithmetic is fp32 products with fp32 accumulation,
-// like the vector-ALU path.
+// contractions with a 16-wide output dimension; the 16x16x4 MFMA forms take
+// their two operands spread over the 64 lanes (one value per lane), so the
+// 16-wide factor (Q rows in the left product, P rows in the right one) never
+// has to be broadcast, and A goes straight from 16-byte global loads into
+// the instruction.  The left product and the reconstruction are fp32
+// products with fp32 accumulation; the right product runs in fp64 (see
+// k_qm).
 //
 // Lane layout of v_mfma_f32_16x16x4_f32 (lane l = 16*g + li):
 //   A operand  a = A[i = li][k = g]      B operand  b = B[k = g][j = li]
@@ -18,11 +19,11 @@
 //          per 4 lanes) and feeds them to 8 MFMAs whose K index is column
 //          8g+j.  The B operand is Q[8g+j][li].  The next K-step's A and Q are
 //          loaded before the current one is used.
-//   k_qm   Q = A^T P_hat partials.  A block owns 128 columns and a row split;
-//          each wave takes a quarter of the rows in 4-row K-steps: lane
-//          (g, li) loads columns 8li..8li+7 of row g and feeds 8 MFMAs, MFMA t
-//          producing the interleaved column tile {8m + t}.  The B operand is
-//          P_hat[row g][li].
+//   k_qm   Q' = A^T P partials (fp64).  A block owns 128 columns and a row
+//          split; each wave takes an eighth of the rows in 4-row K-steps:
+//          lane (g, li) loads columns 8li..8li+7 of row g and feeds 8 MFMAs,
+//          MFMA t producing the interleaved column tile {8m + t}.  The B
+//          operand is P[row g][li].
 //   k_mh16 M_hat = P_hat Q^T and err = A - M_hat (see below).
 #pragma once
 
