@@ -393,7 +393,6 @@ occ_status_t run_batch_t(const Batch& b, void* ws, uint32_t* flags, bool finish,
       }));
     }
   }
-  const dim3 blk(kBlock);
   occ_status_t st = OCC_OK;
   with_rp(b.rp, [&](auto RPc) {
     constexpr int RP = decltype(RPc)::value;
