@@ -248,18 +248,20 @@ __device__ __forceinline__ void pm_tile_issue(const Desc& d, const float* qs, in
 
 // RM (row-sparse step): rows through the row map, register loads only (the
 // tile path's wait counts assume its DMA instructions alone are in flight).
+// Rows [PM_ROWS rb, PM_ROWS (rb + 1)) of P: stored to praw, and as doubles
+// to sm.e.rows (zero past m) for the Gram partial; ends with a barrier.
 template <int DT, bool VEC, int RP, bool RM = false>
-__device__ __forceinline__ void pm_body(const Desc& d, int b, PMSmem& sm) {
+__device__ __forceinline__ void pm_rows(const Desc& d, int rb, PMSmem& sm) {
   const int wave = wave_id(), lane = threadIdx.x & 63;
   const int li = lane & 15, g = lane >> 4;
-  const int row0 = b * PM_ROWS;
+  const int row0 = rb * PM_ROWS;
   const int nk = (d.n + 31) / 32;
   const float* qs = q_src<RP>(d);
 
-  // Blocks start their walk at staggered K-steps (and wrap around), so that
-  // at any moment the device reads many column ranges instead of one stripe
-  // of every row (which lands on a few HBM channels).
-  const int ks0 = (int)(((int64_t)b * PM_WAVES) % nk);
+  // Row blocks start their walk at staggered K-steps (and wrap around), so
+  // that at any moment the device reads many column ranges instead of one
+  // stripe of every row (which lands on a few HBM channels).
+  const int ks0 = (int)(((int64_t)rb * PM_WAVES) % nk);
   auto kcol = [&](int it) {
     int k = ks0 + it;
     if (k >= nk) k -= nk;
@@ -413,7 +415,29 @@ __device__ __forceinline__ void pm_body(const Desc& d, int b, PMSmem& sm) {
     sm.e.rows[i * RP + k] = (i < nr) ? (double)s : 0.0;
   }
   __syncthreads();
-  gram_rows_store<RP, PM_THREADS>(sm.e.rows, nr, d.gpart + (int64_t)b * (RP * (RP + 1) / 2));
+}
+
+// Block b takes row blocks b, b + ng, b + 2 ng, ... (ng = d.ng blocks, at
+// most F_PM_MAXBLOCKS, so that the Gram partials stay few for tall
+// matrices) and stores one packed fp64 Gram partial of all its rows
+// (entry p accumulated by thread p, rows in order).
+template <int DT, bool VEC, int RP, bool RM = false>
+__device__ __forceinline__ void pm_body(const Desc& d, int b, PMSmem& sm) {
+  constexpr int NP = RP * (RP + 1) / 2;
+  static_assert(NP <= PM_THREADS, "one Gram entry per thread");
+  const int t = threadIdx.x;
+  int gk = 0, gl = 0;
+  if (t < NP) upper_entry<RP>(t, gk, gl);
+  double gacc = 0.0;
+  const int row_blocks = (d.m + PM_ROWS - 1) / PM_ROWS;
+  for (int rb = b; rb < row_blocks; rb += d.ng) {
+    if (rb != b) __syncthreads();   // the rows are read before the next tiles land there
+    pm_rows<DT, VEC, RP, RM>(d, rb, sm);
+    const int nr = min(PM_ROWS, d.m - rb * PM_ROWS);
+    if (t < NP)
+      for (int i = 0; i < nr; ++i) gacc = fma(sm.e.rows[i * RP + gk], sm.e.rows[i * RP + gl], gacc);
+  }
+  if (t < NP) d.gpart[(int64_t)b * NP + t] = gacc;
 }
 
 template <int DT, bool VEC, int RP, bool RM = false>

@@ -89,20 +89,6 @@ __device__ __forceinline__ void upper_entry(int p, int& k, int& l) {
   l = kk + rem;
 }
 
-// Gram of `nr` rows held in LDS as doubles (row pitch RP): the packed upper
-// triangle, written to dst[0 .. NP).
-template <int RP, int NT = kBlock>
-__device__ __forceinline__ void gram_rows_store(const double* rows, int nr, double* dst) {
-  constexpr int NP = RP * (RP + 1) / 2;
-  for (int p = threadIdx.x; p < NP; p += NT) {
-    int k, l;
-    upper_entry<RP>(p, k, l);
-    double s = 0.0;
-    for (int i = 0; i < nr; ++i) s = fma(rows[i * RP + k], rows[i * RP + l], s);
-    dst[p] = s;
-  }
-}
-
 // -------------------------------------------------------------------------
 // Orthogonalisation of the small-rank path (Sec. 2.3 CholeskyQR; the second
 // pass only when the first lost orthogonality).  P_hat = P T with
@@ -369,12 +355,14 @@ __device__ __forceinline__ void orth_t_body(const Desc& d, uint32_t* flags, Chol
 
 // -------------------------------------------------------------------------
 // k_qfin16: the factor T applied.  Blocks [0, nq) (kind K_QRED): for
-// kBlock / RP columns c each, Q'[c][k] = sum over row splits of the fp64
-// qpart[s][c][k] (in split order), then Q[c][j] = sum_k Q'[c][k] T[k][j]
-// (fp64, k ascending), written to the caller's Q and the padded copy.
-// Blocks [nq, ...) (kind K_APPLY): for kBlock / RP rows each,
-// P_hat[i][j] = sum_k P[i][k] T[k][j] (fp64, k ascending), written to the
-// caller's P and the padded copy.
+// kBlock / (S RP) columns c each, Q'[c][k] = sum over the sq row splits of
+// the fp64 qpart[s][c][k] -- S = qfin_slices(sq) threads per element each
+// summing a consecutive slice of the splits in order, the slices then added
+// in order -- then Q[c][j] = sum_k Q'[c][k] T[k][j] (fp64, k ascending),
+// written to the caller's Q and the padded copy.
+// Blocks [nq, ...) (kind K_APPLY): for kBlock / (RP / 4) rows each,
+// P_hat[i][j] = sum_k P[i][k] T[k][j] (fp64, k ascending), four columns j per
+// thread, written to the caller's P and the padded copy.
 // -------------------------------------------------------------------------
 template <int RP>
 __device__ __forceinline__ void load_t(const Desc& d, double* Ts) {
@@ -382,27 +370,37 @@ __device__ __forceinline__ void load_t(const Desc& d, double* Ts) {
 }
 
 template <int RP>
-__device__ __forceinline__ void qfin_q_body(const Desc& d, int b, double* Ts, double* qs) {
-  constexpr int CPB = kBlock / RP;
-  const int t = threadIdx.x, cl = t / RP, k = t % RP;
+__device__ __forceinline__ void qfin_q_body(const Desc& d, int b, double* Ts, double* qs,
+                                            double* part) {
+  const int S = qfin_slices(d.sq);
+  const int t = threadIdx.x, o = t / S, sl = t % S;   // element o of the block, slice sl
+  const int cl = o / RP, k = o % RP;
   load_t<RP>(d, Ts);
   const double* qp = (const double*)d.qpart;
-  const int64_t c = (int64_t)b * CPB + cl;
+  const int64_t c = (int64_t)b * (kBlock / (S * RP)) + cl;
   const int64_t idx = c * RP + k;
+  const int per = (d.sq + S - 1) / S;
+  const int s0 = min(d.sq, sl * per), s1 = min(d.sq, s0 + per);
   double acc = 0.0;
   if (c < d.n) {
-    for (int t0 = 0; t0 < d.sq; t0 += 16) {
+    for (int t0 = s0; t0 < s1; t0 += 16) {
       double v[16];
 #pragma unroll
-      for (int u = 0; u < 16; ++u) v[u] = (t0 + u < d.sq) ? qp[(int64_t)(t0 + u) * d.n * RP + idx] : 0.0;
+      for (int u = 0; u < 16; ++u) v[u] = (t0 + u < s1) ? qp[(int64_t)(t0 + u) * d.n * RP + idx] : 0.0;
 #pragma unroll
       for (int u = 0; u < 16; ++u)
-        if (t0 + u < d.sq) acc = (t0 + u == 0) ? v[u] : acc + v[u];
+        if (t0 + u < s1) acc = (t0 + u == s0) ? v[u] : acc + v[u];
     }
   }
-  qs[t] = acc;
+  part[t] = acc;
   __syncthreads();
-  if (c >= d.n) return;
+  if (sl == 0) {
+    double q = part[t];
+    for (int x = 1; x < S; ++x) q = q + part[t + x];
+    qs[o] = q;
+  }
+  __syncthreads();
+  if (sl != 0 || c >= d.n) return;
   double q = 0.0;
 #pragma unroll
   for (int kk = 0; kk < RP; ++kk) q = fma(qs[cl * RP + kk], Ts[kk * RP + k], q);
@@ -413,31 +411,39 @@ __device__ __forceinline__ void qfin_q_body(const Desc& d, int b, double* Ts, do
 
 template <int RP>
 __device__ __forceinline__ void qfin_p_body(const Desc& d, int b, double* Ts) {
-  constexpr int RPB = kBlock / RP;
-  const int t = threadIdx.x, j = t % RP;
+  constexpr int TPR = RP / 4;               // threads per row
+  constexpr int RPB = kBlock / TPR;
+  const int t = threadIdx.x, j0 = 4 * (t % TPR);
   load_t<RP>(d, Ts);
   __syncthreads();
-  const int64_t row = (int64_t)b * RPB + t / RP;
+  const int64_t row = (int64_t)b * RPB + t / TPR;
   if (row >= d.m) return;
   double x[RP];
   p_row<RP>(d, row, x);
-  double acc = 0.0;
+  float out[4];
 #pragma unroll
-  for (int k = 0; k < RP; ++k) acc = fma(x[k], Ts[k * RP + j], acc);
-  const float out = (float)acc;
+  for (int q = 0; q < 4; ++q) {
+    double acc = 0.0;
+#pragma unroll
+    for (int k = 0; k < RP; ++k) acc = fma(x[k], Ts[k * RP + j0 + q], acc);
+    out[q] = (float)acc;
+  }
   // the padded copy is always written: the reconstruction pass reads it
   // with 16-byte loads (the caller's P has no alignment guarantee)
-  d.phat[row * RP + j] = out;
-  if (j < d.r) d.P[row * d.r + j] = out;
+  *(float4*)(d.phat + row * RP + j0) = make_float4(out[0], out[1], out[2], out[3]);
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    if (j0 + q < d.r) d.P[row * d.r + j0 + q] = out[q];
 }
 
 template <int RP>
 __global__ __launch_bounds__(kBlock) void k_qfin16(OCC_KARGS, int nq) {
   __shared__ double Ts[RP * RP];
   __shared__ double qs[kBlock];
+  __shared__ double part[kBlock];
   const int b = (int)blockIdx.x;
   if (b < nq) {
-#define B_(d, bb) qfin_q_body<RP>(d, bb, Ts, qs)
+#define B_(d, bb) qfin_q_body<RP>(d, bb, Ts, qs, part)
     OCC_DISPATCH_AT(K_QRED, B_, b)
 #undef B_
   } else {

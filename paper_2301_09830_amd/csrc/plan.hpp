@@ -94,12 +94,18 @@ inline int padded_rank(int r) {
 // Small-rank path (padded rank <= 16): tile constants shared with
 // kernels_small.hpp and kernels_mfma16.hpp.
 constexpr int kFusedMaxRank = 16;
-constexpr int F_PROWS = 32;       // left product: rows per block
+constexpr int F_PROWS = 32;       // left product: rows per row block
+constexpr int F_PM_MAXBLOCKS = 512;  // left product: blocks (each one Gram partial), at most
 constexpr int F_QCOLS = 128;      // right product: columns per block
 constexpr int F_MHCOLS = 128;     // reconstruction: columns per block
 constexpr int F_MHGROUP = 64;     // reconstruction: rows per block step (4 waves x 16 rows)
 constexpr int F_MHBLOCKS = 1024;  // reconstruction: target number of blocks
 constexpr int F_QBLOCKS = 512;    // right product: resident blocks (2 per CU on 256 CUs)
+// finishing kernel: threads that share the sum of one element's sq row-split
+// partials (each thread at most 32 of them)
+__host__ __device__ constexpr int qfin_slices(int sq) {
+  return sq > 256 ? 16 : sq > 128 ? 8 : sq > 64 ? 4 : sq > 32 ? 2 : 1;
+}
 
 // Large-rank path (padded rank 32, 64, 128): tile constants shared with
 // kernels_large.hpp.
@@ -149,7 +155,7 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0,
     const int64_t p_blocks = cdiv(m, F_PROWS);
     t.sp = 1;
     t.p_cols = (int)round_up(n, 32);
-    t.ng = (int)p_blocks;
+    t.ng = (int)std::min<int64_t>(p_blocks, F_PM_MAXBLOCKS);
     // right product: at most F_QBLOCKS - 1 blocks, so that they and the
     // block forming T run in one round
     const int64_t col_tiles = cdiv(n, F_QCOLS);
@@ -162,10 +168,10 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0,
     const int64_t rbm = clamp64(cdiv(F_MHBLOCKS, ctm), 1, cdiv(m, F_MHGROUP));
     t.mr = (int)round_up(cdiv(m, rbm), F_MHGROUP);
     t.blocks[K_QPAD] = cdiv((int64_t)t.n_pad * rp, kBlock);
-    t.blocks[K_PASS_P] = p_blocks;
+    t.blocks[K_PASS_P] = t.ng;
     t.blocks[K_PASS_Q] = col_tiles * t.sq;   // plus one block per matrix forming T
-    t.blocks[K_QRED] = cdiv(n * rp, kBlock);
-    t.blocks[K_APPLY] = cdiv(m * rp, kBlock);
+    t.blocks[K_QRED] = cdiv(n * rp * qfin_slices(t.sq), kBlock);
+    t.blocks[K_APPLY] = cdiv(m * (rp / 4), kBlock);
     t.blocks[K_MHAT] = ctm * cdiv(m, t.mr);
     return t;
   }
