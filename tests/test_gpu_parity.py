@@ -155,6 +155,25 @@ def test_ill_conditioned_iterates_second_pass(rank, iters, ratio):
     assert_parity(res, "f32", f"geometric {ratio}^-j r{rank} t{iters}")
 
 
+@pytest.mark.parametrize("kind", ["lowrank", "geom"])
+def test_batched_small_rank_split_sums(kind):
+    """One batched small-rank step (one factor block per matrix in the right
+    product's launch) over matrices whose right products have many row
+    splits: 2000, 4000, 8000 and 16000 rows of 96 columns give 63, 125, 250
+    and 500 splits, whose sums the finishing kernel shares over 2, 4, 8 and 16
+    threads per element; 20000 x 96 has more row blocks than left-product
+    blocks (each block takes several); 300 x 257 is wide.  "geom" makes the
+    power iterates of every matrix ill-conditioned enough for the second
+    CholeskyQR pass inside the batch."""
+    shapes = ((2000, 96), (4000, 96), (8000, 96), (16000, 96), (20000, 96), (300, 257))
+    if kind == "lowrank":
+        w = Workload(94, "mixed", shapes, "f32", 8, 2, 2, "lowrank", signal_rank=48, noise=1e-3)
+    else:
+        w = Workload(95, "mixed_geom", shapes, "f32", 8, 2, 2, "geom", signal_rank=16, noise=1.5)
+    res, _, _ = run_workload(w, 2, batched=True)
+    assert_parity(res, "f32", f"batched {kind} r8 t2, {len(shapes)} matrices")
+
+
 @pytest.mark.parametrize("shape,rank,iters", [((20000, 96), 16, 1), ((9000, 130), 8, 2),
                                               ((8193, 64), 4, 1)])
 def test_tall_small_rank_chunked_orthogonalisation(shape, rank, iters):
