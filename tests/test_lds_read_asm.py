@@ -199,23 +199,55 @@ def strongly_connected(n, succ):
     return comps
 
 
-def loop_waits(body):
-    """For each loop holding hand-written vmcnt waits: (waits, vector-memory
-    instructions per iteration)."""
-    blocks, succ = basic_blocks(body)
+def loops(blocks_in, succ, preds):
+    """Every loop of the control-flow graph restricted to `blocks_in`, nested
+    loops included: each nontrivial strongly connected component, then,
+    with the edges back into its header removed (the block entered from
+    outside it, else its first block), the loops inside it."""
+    idx = sorted(blocks_in)
+    pos = {b: i for i, b in enumerate(idx)}
+    sub = [[pos[w] for w in succ[b] if w in pos] for b in idx]
     out = []
-    for comp in strongly_connected(len(blocks), succ):
-        if len(comp) == 1 and comp[0] not in succ[comp[0]]:
-            continue
-        waits = set()
-        for b in comp:
+    for comp in strongly_connected(len(idx), sub):
+        members = {idx[i] for i in comp}
+        if len(members) == 1:
+            b = next(iter(members))
+            if b not in succ[b]:
+                continue
+        out.append(members)
+        entries = [b for b in members if any(p not in members for p in preds[b])]
+        header = min(entries) if entries else min(members)
+        inner_succ = {b: [w for w in succ[b] if w != header] for b in members}
+        full = [inner_succ.get(b, []) for b in range(len(succ))]
+        out.extend(loops(members - {header}, full, preds))
+    return out
+
+
+def loop_waits(body):
+    """For each innermost loop holding hand-written vmcnt waits: (waits,
+    vector-memory instructions per iteration)."""
+    blocks, succ = basic_blocks(body)
+    preds = [[] for _ in blocks]
+    for v, ws in enumerate(succ):
+        for w in ws:
+            preds[w].append(v)
+
+    def waits_of(members):
+        found = set()
+        for b in members:
             ins = blocks[b][1]
             for j, t in enumerate(ins):
                 m = re.match(r"s_waitcnt vmcnt\((\d+)\)$", t)
                 if m and j > 0 and ins[j - 1].startswith(";;#ASMSTART"):
-                    waits.add(int(m.group(1)))
-        if any(waits):
-            out.append((sorted(waits), sum(1 for b in comp for t in blocks[b][1] if VMEM.match(t))))
+                    found.add(int(m.group(1)))
+        return found
+
+    with_waits = [c for c in loops(set(range(len(blocks))), succ, preds) if any(waits_of(c))]
+    out = []
+    for c in with_waits:
+        if any(o < c and waits_of(o) == waits_of(c) for o in with_waits):
+            continue   # a loop nested in this one holds the same waits
+        out.append((sorted(waits_of(c)), sum(1 for b in c for t in blocks[b][1] if VMEM.match(t))))
     return out
 
 
@@ -253,6 +285,13 @@ def test_wait_scan_flags_a_drifted_count():
     assert wait_violations(functions(drifted))[1]
     spilled = good[:2] + ["scratch_load_dword v9, off, s32"] + good[2:]
     assert wait_violations(functions(spilled))[1]
+    # the same loop nested in an outer loop that issues other loads: the
+    # inner loop is the one checked
+    nested = (good[:1] + [".LBB0_0:", "global_load_dwordx4 v[4:7], v[2:3], off"] + good[1:-2]
+              + ["global_store_dword v[2:3], v4, off", "s_cbranch_scc1 .LBB0_0", "s_endpgm", ".Lfunc_end0:"])
+    assert wait_violations(functions(nested)) == ({"_ZN3occ4k_pmXE"}, [])
+    nested_drifted = [ln.replace("vmcnt(6)", "vmcnt(8)").replace("vmcnt(3)", "vmcnt(4)") for ln in nested]
+    assert wait_violations(functions(nested_drifted))[1]
 
 
 @pytest.mark.skipif(not HAVE_HIPCC, reason="hipcc not available")
