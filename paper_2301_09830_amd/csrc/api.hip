@@ -413,7 +413,12 @@ occ_status_t run_batch_t(const Batch& b, void* ws, uint32_t* flags, bool finish,
         if (b.fused) {
           if (b.descs[0].r != RP) L("qpad", k_qpad<RP>, b.blocks[K_QPAD]);
           for (int it = 0; it < b.iters; ++it) {
-            LB("pass_p", k_pm<DT, VEC, RP, RM>, b.blocks[K_PASS_P], PM_THREADS);
+            bool narrow = false;   // a matrix with fewer 32-column K-steps than waves
+            for (const Desc& dd : b.descs) narrow = narrow || pm_waves_per_rb(dd.n) < PM_WAVES;
+            if (narrow)
+              LB("pass_p", k_pm<DT, VEC, RP, RM, true>, b.blocks[K_PASS_P], PM_THREADS);
+            else
+              LB("pass_p", k_pm<DT, VEC, RP, RM>, b.blocks[K_PASS_P], PM_THREADS);
             // T of each matrix (first `count` blocks) beside Q' = A^T P
             LB("pass_q", k_qm<DT, VEC, RP, RM>, count + b.blocks[K_PASS_Q], QM_THREADS, flags);
             L("q_finish", k_qfin16<RP>, b.blocks[K_QRED] + b.blocks[K_APPLY],

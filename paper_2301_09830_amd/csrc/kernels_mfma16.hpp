@@ -58,7 +58,7 @@ __device__ __forceinline__ float lds_elem(const typename LdsVec<W>::T& v, int j)
 
 constexpr int PM_RB = 2;                  // 16-row MFMA tiles per block in k_pm
 constexpr int PM_ROWS = 16 * PM_RB;       // rows per block (== F_PROWS)
-constexpr int PM_WAVES = 4;               // waves per block in k_pm
+constexpr int PM_WAVES = F_PM_WAVES;      // waves per block in k_pm
 constexpr int PM_THREADS = PM_WAVES * kWave;
 static_assert(PM_ROWS == F_PROWS, "k_pm block rows must match the plan");
 constexpr int QM_COLS = F_QCOLS;          // columns per block in k_qm
@@ -155,11 +155,12 @@ __device__ __forceinline__ Q8v q8_load(const float* qs, int n, int c, int li) {
 }
 
 // -------------------------------------------------------------------------
-// k_pm: left product on MFMA.  A block owns PM_ROWS whole rows; its
-// PM_WAVES waves take interleaved 32-column K-steps of those rows (so
-// together they stream contiguous column ranges) and their partial tiles are
-// summed in LDS in wave order.  The block then stores its final rows of P and the fp64
-// Gram partial of those rows.
+// k_pm: left product on MFMA.  A block owns PM_ROWS whole rows at a time;
+// its PM_WAVES waves take interleaved 32-column K-steps of those rows (so
+// together they stream contiguous column ranges; a matrix with fewer K-steps
+// than waves has the spare waves take the next row blocks) and their partial
+// tiles are summed in LDS in wave order.  The block stores the final rows of
+// P and accumulates the fp64 Gram partial of all its rows.
 //
 // The MFMA operand layout gives each of a load's 64 lanes a different row
 // out of 16 (4 lanes x 16 bytes per row), so a load straight into registers
@@ -191,7 +192,7 @@ constexpr int PM_STAGES = 3;             // K-step stages per wave (two in fligh
 union PMSmem {
   struct {
     float red[PM_WAVES][PM_ROWS * 16];   // per-wave partial tiles
-    double rows[PM_ROWS * 16];           // final P rows as doubles (Gram)
+    double rows[PM_WAVES * PM_ROWS * 16];   // final P rows of the group as doubles (Gram)
   } e;
   uint8_t tile[PM_WAVES][PM_STAGES][pm_stage<DT_F32>()];   // per wave, the K-step stages
 };
@@ -248,20 +249,27 @@ __device__ __forceinline__ void pm_tile_issue(const Desc& d, const float* qs, in
 
 // RM (row-sparse step): rows through the row map, register loads only (the
 // tile path's wait counts assume its DMA instructions alone are in flight).
-// Rows [PM_ROWS rb, PM_ROWS (rb + 1)) of P: stored to praw, and as doubles
-// to sm.e.rows (zero past m) for the Gram partial; ends with a barrier.
-template <int DT, bool VEC, int RP, bool RM = false>
-__device__ __forceinline__ void pm_rows(const Desc& d, int rb, PMSmem& sm) {
+// Row group grp of P: row blocks grp * rpg .. grp * rpg + rpg - 1 (rpg =
+// PM_WAVES / wk), wave w taking row block grp * rpg + w / wk and its K-steps
+// w % wk, w % wk + wk, ... (wk = pm_waves_per_rb(n) waves per row block).
+// The rows are stored to praw, and as doubles to sm.e.rows (zero past m)
+// for the Gram partial; ends with a barrier.
+template <int DT, bool VEC, int RP, bool RM, int WK>
+__device__ __forceinline__ void pm_rows(const Desc& d, int grp, PMSmem& sm) {
   const int wave = wave_id(), lane = threadIdx.x & 63;
   const int li = lane & 15, g = lane >> 4;
-  const int row0 = rb * PM_ROWS;
   const int nk = (d.n + 31) / 32;
+  constexpr int wk = WK, rpg = PM_WAVES / WK;
+  const int row_blocks = (d.m + PM_ROWS - 1) / PM_ROWS;
+  const int rb = grp * rpg + wave / wk, kw = wave % wk;
+  const bool live = rb < row_blocks;
+  const int row0 = rb * PM_ROWS;
   const float* qs = q_src<RP>(d);
 
   // Row blocks start their walk at staggered K-steps (and wrap around), so
   // that at any moment the device reads many column ranges instead of one
   // stripe of every row (which lands on a few HBM channels).
-  const int ks0 = (int)(((int64_t)rb * PM_WAVES) % nk);
+  const int ks0 = (int)(((int64_t)rb * wk) % nk);
   auto kcol = [&](int it) {
     int k = ks0 + it;
     if (k >= nk) k -= nk;
@@ -290,7 +298,7 @@ __device__ __forceinline__ void pm_rows(const Desc& d, int rb, PMSmem& sm) {
   if constexpr (VEC && !RM) {
     dma = d.err_in != nullptr && (d.n & 31) == 0 && ((uintptr_t)qs & 15) == 0;
     if (dma) {
-      // This wave's K-steps ks = wave + PM_WAVES * it; step it lives in stage
+      // This wave's K-steps ks = kw + wk * it; step it lives in stage
       // it % PM_STAGES.  Per step: wait until only the steps issued after it
       // may be in flight, read its operands (inline ds_read, see above),
       // issue the step PM_STAGES - 1 ahead into the stage just freed, run the
@@ -300,10 +308,10 @@ __device__ __forceinline__ void pm_rows(const Desc& d, int rb, PMSmem& sm) {
       static_assert(PM_STAGES <= 4 && 2 * NI <= 63, "vmcnt immediates");
       uint8_t* const tiles = sm.tile[wave][0];
       const uint32_t tbase = (uint32_t)(size_t)(lvoid_t*)tiles;
-      const int nmine = wave < nk ? (nk - wave + PM_WAVES - 1) / PM_WAVES : 0;
+      const int nmine = live && kw < nk ? (nk - kw + wk - 1) / wk : 0;
 #pragma unroll
       for (int y = 0; y + 1 < PM_STAGES; ++y)
-        if (y < nmine) pm_tile_issue<DT, RP>(d, qs, row0, kcol(wave + PM_WAVES * y) - 8 * g, tiles + y * STAGE);
+        if (y < nmine) pm_tile_issue<DT, RP>(d, qs, row0, kcol(kw + wk * y) - 8 * g, tiles + y * STAGE);
       int st = 0;
       for (int it = 0; it < nmine; ++it) {
         const int after = min(it + PM_STAGES - 2, nmine - 1) - it;
@@ -346,7 +354,7 @@ __device__ __forceinline__ void pm_rows(const Desc& d, int rb, PMSmem& sm) {
         }
         if (it + PM_STAGES - 1 < nmine) {
           const int sn = st == 0 ? PM_STAGES - 1 : st - 1;
-          pm_tile_issue<DT, RP>(d, qs, row0, kcol(wave + PM_WAVES * (it + PM_STAGES - 1)) - 8 * g,
+          pm_tile_issue<DT, RP>(d, qs, row0, kcol(kw + wk * (it + PM_STAGES - 1)) - 8 * g,
                                 tiles + sn * STAGE);
         }
         st = st + 1 == PM_STAGES ? 0 : st + 1;
@@ -374,16 +382,16 @@ __device__ __forceinline__ void pm_rows(const Desc& d, int rb, PMSmem& sm) {
   if (!dma) {
     Ch8<DT> cur[PM_RB], nxt[PM_RB];
     Q8v cq, nq;
-    int ks = wave;
+    int ks = live ? kw : nk;
     if (ks < nk) {
       const int c = kcol(ks);
       cq = q8_load<RP>(qs, d.n, c, li);
 #pragma unroll
       for (int r = 0; r < PM_RB; ++r) cur[r] = ch8_load<DT, VEC, RM>(d, row0 + 16 * r + li, c, d.n);
     }
-    for (; ks < nk; ks += PM_WAVES) {
-      const bool more = ks + PM_WAVES < nk;
-      const int cn = more ? kcol(ks + PM_WAVES) : 0;
+    for (; ks < nk; ks += wk) {
+      const bool more = ks + wk < nk;
+      const int cn = more ? kcol(ks + wk) : 0;
       if (more) {
         nq = q8_load<RP>(qs, d.n, cn, li);
 #pragma unroll
@@ -405,23 +413,26 @@ __device__ __forceinline__ void pm_rows(const Desc& d, int rb, PMSmem& sm) {
 #pragma unroll
     for (int v = 0; v < 4; ++v) sm.e.red[wave][(16 * r + 4 * g + v) * 16 + li] = acc[r][v];
   __syncthreads();
-  const int nr = min(PM_ROWS, d.m - row0);
-  for (int e = threadIdx.x; e < PM_ROWS * RP; e += PM_THREADS) {
-    const int i = e / RP, k = e % RP;
-    float s = sm.e.red[0][i * 16 + k];
+  // row block r of the group: the partial tiles of waves r wk .. r wk + wk - 1, in order
+  for (int e = threadIdx.x; e < rpg * PM_ROWS * RP; e += PM_THREADS) {
+    const int r = e / (PM_ROWS * RP), i = (e / RP) % PM_ROWS, k = e % RP;
+    float s = sm.e.red[r * wk][i * 16 + k];
 #pragma unroll
-    for (int w = 1; w < PM_WAVES; ++w) s = s + sm.e.red[w][i * 16 + k];
-    if (i < nr) d.praw[(int64_t)(row0 + i) * RP + k] = s;
-    sm.e.rows[i * RP + k] = (i < nr) ? (double)s : 0.0;
+    for (int w = 1; w < wk; ++w) s = s + sm.e.red[r * wk + w][i * 16 + k];
+    const int64_t row = (int64_t)(grp * rpg + r) * PM_ROWS + i;
+    if (row < d.m) d.praw[row * RP + k] = s;
+    sm.e.rows[(r * PM_ROWS + i) * RP + k] = row < d.m ? (double)s : 0.0;
   }
   __syncthreads();
 }
 
-// Block b takes row blocks b, b + ng, b + 2 ng, ... (ng = d.ng blocks, at
+// Block b takes row groups b, b + ng, b + 2 ng, ... (ng = d.ng blocks, at
 // most F_PM_MAXBLOCKS, so that the Gram partials stay few for tall
 // matrices) and stores one packed fp64 Gram partial of all its rows
-// (entry p accumulated by thread p, rows in order).
-template <int DT, bool VEC, int RP, bool RM = false>
+// (entry p accumulated by thread p, rows in order).  NARROW: some matrix of
+// the launch has fewer K-steps than waves (each matrix's row grouping is
+// chosen at run time); otherwise every matrix takes one row block at a time.
+template <int DT, bool VEC, int RP, bool RM = false, bool NARROW = false>
 __device__ __forceinline__ void pm_body(const Desc& d, int b, PMSmem& sm) {
   constexpr int NP = RP * (RP + 1) / 2;
   static_assert(NP <= PM_THREADS, "one Gram entry per thread");
@@ -429,21 +440,24 @@ __device__ __forceinline__ void pm_body(const Desc& d, int b, PMSmem& sm) {
   int gk = 0, gl = 0;
   if (t < NP) upper_entry<RP>(t, gk, gl);
   double gacc = 0.0;
-  const int row_blocks = (d.m + PM_ROWS - 1) / PM_ROWS;
-  for (int rb = b; rb < row_blocks; rb += d.ng) {
-    if (rb != b) __syncthreads();   // the rows are read before the next tiles land there
-    pm_rows<DT, VEC, RP, RM>(d, rb, sm);
-    const int nr = min(PM_ROWS, d.m - rb * PM_ROWS);
+  const int wk = NARROW ? pm_waves_per_rb(d.n) : PM_WAVES, rpg = PM_WAVES / wk;
+  const int row_groups = ((d.m + PM_ROWS - 1) / PM_ROWS + rpg - 1) / rpg;
+  for (int grp = b; grp < row_groups; grp += d.ng) {
+    if (grp != b) __syncthreads();   // the rows are read before the next tiles land there
+    if (!NARROW || wk == PM_WAVES) pm_rows<DT, VEC, RP, RM, PM_WAVES>(d, grp, sm);
+    else if (wk == 2) pm_rows<DT, VEC, RP, RM, 2>(d, grp, sm);
+    else pm_rows<DT, VEC, RP, RM, 1>(d, grp, sm);
+    const int nr = min(rpg * PM_ROWS, d.m - grp * rpg * PM_ROWS);
     if (t < NP)
       for (int i = 0; i < nr; ++i) gacc = fma(sm.e.rows[i * RP + gk], sm.e.rows[i * RP + gl], gacc);
   }
   if (t < NP) d.gpart[(int64_t)b * NP + t] = gacc;
 }
 
-template <int DT, bool VEC, int RP, bool RM = false>
+template <int DT, bool VEC, int RP, bool RM = false, bool NARROW = false>
 __global__ __launch_bounds__(PM_THREADS) void k_pm(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) PMSmem sm;
-#define B_(d, b) pm_body<DT, VEC, RP, RM>(d, b, sm)
+#define B_(d, b) pm_body<DT, VEC, RP, RM, NARROW>(d, b, sm)
   OCC_DISPATCH(K_PASS_P, B_)
 #undef B_
 }

@@ -96,6 +96,11 @@ inline int padded_rank(int r) {
 constexpr int kFusedMaxRank = 16;
 constexpr int F_PROWS = 32;       // left product: rows per row block
 constexpr int F_PM_MAXBLOCKS = 512;  // left product: blocks (each one Gram partial), at most
+constexpr int F_PM_WAVES = 4;        // left product: waves per block
+// left product: waves sharing one row block's 32-column K-steps, all of
+// them unless the matrix has fewer K-steps than waves (n <= 96); the other
+// waves of the block take the next row blocks
+__host__ __device__ constexpr int pm_waves_per_rb(int n) { return n > 96 ? 4 : (n > 32 ? 2 : 1); }
 constexpr int F_QCOLS = 128;      // right product: columns per block
 constexpr int F_MHCOLS = 128;     // reconstruction: columns per block
 constexpr int F_MHGROUP = 64;     // reconstruction: rows per block step (4 waves x 16 rows)
@@ -155,7 +160,8 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0,
     const int64_t p_blocks = cdiv(m, F_PROWS);
     t.sp = 1;
     t.p_cols = (int)round_up(n, 32);
-    t.ng = (int)std::min<int64_t>(p_blocks, F_PM_MAXBLOCKS);
+    const int64_t p_groups = cdiv(p_blocks, F_PM_WAVES / pm_waves_per_rb((int)n));
+    t.ng = (int)std::min<int64_t>(p_groups, F_PM_MAXBLOCKS);
     // right product: at most F_QBLOCKS - 1 blocks, so that they and the
     // block forming T run in one round
     const int64_t col_tiles = cdiv(n, F_QCOLS);
