@@ -299,6 +299,7 @@ occ_status_t plan_batch(const occ_mat_t* mats, int count, int rank, int iters, u
     d.q_rows = t.q_rows;
     d.m_pad = t.m_pad;
     d.mr = t.mr;
+    d.qr_cols = t.qr_cols;
     d.fused = b.fused ? 1 : 0;
     for (int k = 0; k < K_NUM; ++k) {
       d.blk[k] = (int32_t)b.blocks[k];

@@ -237,45 +237,47 @@ constexpr double kSecondPassCond = 1e3;
 
 // ---------------------------------------------------------------------------
 // Large-rank path: Q padding (k_qpadl) and the Q reduction (k_qredl) over
-// 32-column tiles.  Both write qpad (n_pad x RP) and, when M is bf16, Q as
+// column tiles.  Both write qpad (n_pad x RP) and, when M is bf16, Q as
 // two bf16 parts hi = bf16(v), lo = bf16(v - hi) (v - hi - lo is below
 // 2^-16 |v|) in qbf, transposed so that the left product stages 32 columns
 // of a rank row with 16-byte copies: rank k goes to row (k % NU) * 32 + k / NU,
 // NU = RP / 32, the order in which that kernel's lanes read them.  The
-// transpose goes through LDS, so each qbf row is written in 64-byte runs.
-// k_qpadl covers all n_pad columns (zeros past n); k_qredl sums the row-split
-// partials (fixed order) for the n real columns and also writes the caller's Q.
+// transpose goes through LDS, so each qbf row is written in 16-byte chunks.
+// k_qpadl covers all n_pad columns (zeros past n) in 32-column tiles;
+// k_qredl sums the row-split partials (fixed order, 16 loads in flight per
+// element) for the n real columns, in tiles of d.qr_cols columns (8 or 32),
+// and also writes the caller's Q.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ uint16_t bf16_bits(__bf16 h) { return __builtin_bit_cast(uint16_t, h); }
 
-constexpr int QT_COLS = 32;                 // columns per block
-constexpr int QT_P = QT_COLS;               // LDS pitch (bf16) of a transposed rank row
-constexpr int QT_CH = QT_COLS / 8;          // 16-byte chunks of a transposed rank row
+constexpr int QT_COLS = 32;                 // columns per block, at most
 
 template <int RP>
 struct QTSmem {
-  uint16_t t[2][RP * QT_P];
+  uint16_t t[2][RP * QT_COLS];
 };
 
 template <int RP, bool REDUCE>
 __device__ __forceinline__ void qtile_body(const Desc& d, int b, QTSmem<RP>& sm) {
   constexpr int NU = RP / 32;
-  const int c0 = b * QT_COLS;
+  const int QT_P = REDUCE ? d.qr_cols : QT_COLS;   // columns of this tile = LDS pitch (bf16)
+  const int QT_CH = QT_P / 8;                      // 16-byte chunks of a transposed rank row
+  const int c0 = b * QT_P;
   const int c_end = REDUCE ? d.n : d.n_pad;
-  for (int e = threadIdx.x; e < QT_COLS * RP; e += kBlock) {
+  for (int e = threadIdx.x; e < QT_P * RP; e += kBlock) {
     const int c = c0 + e / RP, k = e % RP;
     if (c >= c_end) continue;
     const int64_t idx = (int64_t)c * RP + k;
     float v;
     if (REDUCE) {
-      // fixed order; loads issued in batches of 8
+      // fixed order; loads issued in batches of 16
       v = 0.f;
-      for (int s0 = 0; s0 < d.sq; s0 += 8) {
-        float p[8];
+      for (int s0 = 0; s0 < d.sq; s0 += 16) {
+        float p[16];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) p[u] = (s0 + u < d.sq) ? d.qpart[(int64_t)(s0 + u) * d.n * RP + idx] : 0.f;
+        for (int u = 0; u < 16; ++u) p[u] = (s0 + u < d.sq) ? d.qpart[(int64_t)(s0 + u) * d.n * RP + idx] : 0.f;
 #pragma unroll
-        for (int u = 0; u < 8; ++u)
+        for (int u = 0; u < 16; ++u)
           if (s0 + u < d.sq) v = (s0 + u == 0) ? p[u] : v + p[u];
       }
       if (k < d.r) d.Q[(int64_t)c * d.r + k] = v;

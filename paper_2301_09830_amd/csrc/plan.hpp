@@ -73,11 +73,12 @@ struct Desc {
   int32_t m_pad;         // large-rank path: rows of phat_t (multiple of 32)
   int32_t mr;            // rows per block of the reconstruction pass
   int32_t vec;           // large-rank path: 16-byte vector loads allowed
+  int32_t qr_cols;       // large-rank path: columns per block of the Q reduction (8 or 32)
 };
 
 // Tiling of one matrix (host side).
 struct Tiling {
-  int sp, p_cols, ng, grows, sq, q_rows, n_pad, m_pad, mr;
+  int sp, p_cols, ng, grows, sq, q_rows, n_pad, m_pad, mr, qr_cols;
   int64_t blocks[K_NUM];
 };
 
@@ -153,6 +154,7 @@ inline int64_t whole_rounds(int64_t want, int64_t slots) {
 inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0,
                           const Slots& sl = Slots{}, bool x3 = false) {
   Tiling t{};
+  t.qr_cols = 32;
   t.n_pad = (int)round_up(n, 32);
   t.m_pad = (int)round_up(m, 32);
   if (rp <= kFusedMaxRank) {
@@ -239,7 +241,13 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0,
   t.blocks[K_GRAM2] = t.ng;
   t.blocks[K_APPLY] = cdiv(m, L_AROWS);
   t.blocks[K_PASS_Q] = ctq * t.sq;
-  t.blocks[K_QRED] = cdiv(n, 32);         // 32-column tiles (k_qredl)
+  // Q reduction: 32-column tiles, or 8-column ones (four times the blocks)
+  // where 32-column tiles would leave this matrix's share of one round of
+  // resident blocks mostly empty: each element sums sq partials, so few
+  // blocks serialise the whole sq x n x rp read (51200 x 3072 at rank 64:
+  // 100 partials, 96 blocks; 50 -> 16 us)
+  t.qr_cols = cdiv(n, 32) < (int64_t)(share * 512.0) ? 8 : 32;
+  t.blocks[K_QRED] = cdiv(n, t.qr_cols);
   t.blocks[K_MHAT] = ctm * cdiv(m, t.mr);
   return t;
 }
