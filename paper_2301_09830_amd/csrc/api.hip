@@ -551,6 +551,7 @@ occ_status_t decompress_impl(const float* P, const float* Q, int64_t m, int64_t 
   d.mr = t.mr;
   // 4 consecutive elements per vector store: 16 bytes (fp32) or 8 (bf16)
   const bool vec = aligned(M_hat, 4 * es) && ldh % 4 == 0;
+  d.vec = vec ? 1 : 0;
   occ_status_t st = OCC_OK;
   with_rp(rp, [&](auto RPc) {
     constexpr int RP = decltype(RPc)::value;

@@ -36,7 +36,8 @@
 //             8-row step through LDS.
 //   k_ml      M_hat = P_hat Q^T and err = A - M_hat; a wave keeps its Q
 //             columns in registers and walks 32-row tiles whose P_hat block
-//             is staged (transposed) in LDS.
+//             is staged (transposed) in LDS; at padded rank 64 the outputs
+//             pass through LDS to be stored by rows.
 #pragma once
 
 #include <type_traits>
@@ -1688,10 +1689,143 @@ __global__ __launch_bounds__(kBlock) void k_lqx(OCC_KARGS) {
 
 // One element of M_hat, nontemporal: fp32, or bf16 (round to nearest even)
 // when OUTBF (stand-alone decompression only).
-template <bool OUTBF>
-__device__ __forceinline__ void store_mhat_nt(const Desc& d, int64_t off, float v) {
-  if constexpr (OUTBF) __builtin_nontemporal_store(bf16_rne(v), (uint16_t*)d.Mhat + off);
-  else __builtin_nontemporal_store(v, d.Mhat + off);
+// -------------------------------------------------------------------------
+// Epilogue of the reconstruction passes (k_ml, k_mlx).  The products leave
+// each 32 x 32 tile of M_hat in the 32x32 MFMA layout: lane (g, li) holds
+// column li of rows mf32_row(v, g), so stores straight from it cover each
+// row in 128-byte pieces of 4-byte accesses.  Each tile goes through LDS
+// instead, and each lane then takes 16-byte pieces of rows: the stored A is
+// read, and M_hat and err written, with 16-byte accesses when the rows are
+// 16-byte aligned (d.vec).  The values are unchanged; only which lane
+// stores which element.
+// -------------------------------------------------------------------------
+constexpr int LE_PITCH = 32 + 4;          // LDS row pitch (floats), 16-byte skew per row
+constexpr int LE_RPI = kWave / 8;         // rows per wave instruction (8 lanes x 16 bytes a row)
+constexpr int LE_IT = 32 / LE_RPI;        // instructions per 32 x 32 tile
+
+// A (the stored fp32 A, compact rows) for this lane's pieces of the tiles
+// of columns cw + 32 c, c < NCT
+template <int NCT>
+__device__ __forceinline__ void lm_epi_load(const Desc& d, bool vec, int row0, int r_hi, int cw,
+                                            f4v (&a4)[NCT][LE_IT]) {
+  const int lane = threadIdx.x & 63;
+  const int rr = lane >> 3;
+#pragma unroll
+  for (int c = 0; c < NCT; ++c) {
+    const int col = cw + 32 * c + 4 * (lane & 7);
+#pragma unroll
+    for (int it = 0; it < LE_IT; ++it) {
+      const int row = row0 + it * LE_RPI + rr;
+      const float* src = d.err_out + (int64_t)row * d.lde_out + col;
+      f4v v = f4v{0.f, 0.f, 0.f, 0.f};
+      if (row < r_hi) {
+        if (vec && col + 4 <= d.n) {
+          v = *(const f4v*)src;
+        } else {
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (col + j < d.n) v[j] = src[j];
+        }
+      }
+      a4[c][it] = v;
+    }
+  }
+}
+
+// The tiles acc[c][v] = M_hat[row0 + mf32_row(v, g)][cw + 32 c + li], one
+// at a time through LDS (ep: this wave's 32 x LE_PITCH floats), then M_hat
+// and err = A - M_hat stored by rows, nontemporal.
+template <int NCT, bool WM, bool WE, bool OUTBF, bool RM>
+__device__ __forceinline__ void lm_epi_store(const Desc& d, bool vec, int row0, int r_hi, int cw,
+                                             const f16v (&acc)[NCT], const f4v (&a4)[NCT][LE_IT],
+                                             float* ep) {
+  typedef float nt4 __attribute__((ext_vector_type(4)));
+  typedef uint32_t nu2 __attribute__((ext_vector_type(2)));
+  const int lane = threadIdx.x & 63;
+  const int li = lane & 31, g = lane >> 5;
+  const int rr = lane >> 3, cq = lane & 7;
+#pragma unroll
+  for (int c = 0; c < NCT; ++c) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) ep[mf32_row(v, g) * LE_PITCH + li] = acc[c][v];
+    // the tile is written and read by this wave only; LDS keeps a wave's
+    // operations in order, and the wait also orders them for the compiler
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    const int col = cw + 32 * c + 4 * cq;
+    const bool vec_col = vec && col + 4 <= d.n;
+#pragma unroll
+    for (int it = 0; it < LE_IT; ++it) {
+      const int tr = it * LE_RPI + rr;
+      const int row = row0 + tr;
+      const f4v mh = *(const f4v*)(ep + tr * LE_PITCH + 4 * cq);
+      if (row >= r_hi || col >= d.n) continue;
+      const int64_t pr = prow<RM>(d, row);
+      float e[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) e[j] = WE ? a4[c][it][j] - mh[j] : 0.f;
+      float* eo = RM ? d.err_fin + pr * d.lde_fin + col : d.err_out + pr * d.lde_out + col;
+      if (vec_col) {
+        if (WM && OUTBF)
+          __builtin_nontemporal_store(nu2{bf16_pack2(mh[0], mh[1]), bf16_pack2(mh[2], mh[3])},
+                                      (nu2*)((uint16_t*)d.Mhat + pr * d.ldh + col));
+        else if (WM)
+          __builtin_nontemporal_store(nt4{mh[0], mh[1], mh[2], mh[3]}, (nt4*)(d.Mhat + pr * d.ldh + col));
+        if (WE) __builtin_nontemporal_store(nt4{e[0], e[1], e[2], e[3]}, (nt4*)eo);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (col + j < d.n) {
+            if (WM) store_mhat1<OUTBF>(d, pr * d.ldh + col + j, mh[j]);
+            if (WE) eo[j] = e[j];
+          }
+        }
+      }
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  }
+}
+
+// The same outputs stored straight from the MFMA layout (4-byte accesses,
+// 128-byte pieces of rows), with A read the same way beforehand (av).
+// Measured faster than the LDS epilogue at padded rank 32 (two tiles per
+// wave) and for the bf16 reconstruction at rank 128.
+template <int NCT>
+__device__ __forceinline__ void lm_direct_load(const Desc& d, int row0, int cw, float (&av)[NCT][16]) {
+  const int lane = threadIdx.x & 63;
+  const int li = lane & 31, g = lane >> 5;
+#pragma unroll
+  for (int c = 0; c < NCT; ++c)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int row = row0 + mf32_row(v, g), col = cw + 32 * c + li;
+      av[c][v] = (row < d.m && col < d.n) ? d.err_out[(int64_t)row * d.lde_out + col] : 0.f;
+    }
+}
+
+template <int NCT, bool WM, bool WE, bool OUTBF, bool RM>
+__device__ __forceinline__ void lm_direct_store(const Desc& d, int row0, int r_hi, int cw,
+                                                const f16v (&acc)[NCT], const float (&av)[NCT][16]) {
+  const int lane = threadIdx.x & 63;
+  const int li = lane & 31, g = lane >> 5;
+#pragma unroll
+  for (int c = 0; c < NCT; ++c) {
+    const int col = cw + 32 * c + li;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int row = row0 + mf32_row(v, g);
+      if (row < r_hi && col < d.n) {
+        const float mh = acc[c][v];
+        const int64_t pr = prow<RM>(d, row);
+        if (WM) {
+          if constexpr (OUTBF) __builtin_nontemporal_store(bf16_rne(mh), (uint16_t*)d.Mhat + pr * d.ldh + col);
+          else __builtin_nontemporal_store(mh, d.Mhat + pr * d.ldh + col);
+        }
+        if (WE)
+          __builtin_nontemporal_store(av[c][v] - mh, RM ? d.err_fin + pr * d.lde_fin + col
+                                                        : d.err_out + pr * d.lde_out + col);
+      }
+    }
+  }
 }
 
 // -------------------------------------------------------------------------
@@ -1703,6 +1837,7 @@ __device__ __forceinline__ void store_mhat_nt(const Desc& d, int64_t off, float 
 template <int RP>
 struct LMSmem {
   float p[2][RP][32];   // P_hat tile, transposed: [rank][row]
+  float ep[lm_lds_epilogue(RP) ? kBlock / kWave : 0][32 * LE_PITCH];   // epilogue tile per wave
 };
 
 template <int RP, int SRC>
@@ -1716,7 +1851,10 @@ __device__ __forceinline__ void lm_stage_direct(const Desc& d, int row0, float (
 
 template <int DT, int RP, int SA, int SRC, bool WM, bool WE, bool OUTBF = false, bool RM = false>
 __device__ __forceinline__ void lm_body(const Desc& d, int b, LMSmem<RP>& sm) {
+  static_assert(!WE || SA == SA_SAVED, "the residual is formed from the stored A");
   constexpr int NCT = lm_tiles(RP), KP = RP / 2, BC = lm_block_cols(RP);
+  constexpr bool EPI = lm_lds_epilogue(RP);
+  const bool vec = d.vec != 0;
   constexpr int SF = RP * 8 / kBlock;   // float4s per thread per P_hat tile
   const int wave = wave_id(), lane = threadIdx.x & 63;
   const int li = lane & 31, g = lane >> 5;
@@ -1768,13 +1906,11 @@ __device__ __forceinline__ void lm_body(const Desc& d, int b, LMSmem<RP>& sm) {
       }
     }
     // A for this tile's outputs (issued before the products to hide latency)
-    RawA<DT, SA, 1> av[NCT][16];
+    f4v a4[EPI ? NCT : 1][LE_IT];
+    float av[EPI ? 1 : NCT][16];
     if (WE) {
-#pragma unroll
-      for (int c = 0; c < NCT; ++c)
-#pragma unroll
-        for (int v = 0; v < 16; ++v)
-          av[c][v] = rawa_load<DT, SA, 1, RM>(d, true, row0 + mf32_row(v, g), cw + 32 * c + li, d.n);
+      if constexpr (EPI) lm_epi_load<NCT>(d, vec, row0, r_hi, cw, a4);
+      else lm_direct_load<NCT>(d, row0, cw, av);
     }
     f16v acc[NCT];
 #pragma unroll
@@ -1786,24 +1922,8 @@ __device__ __forceinline__ void lm_body(const Desc& d, int b, LMSmem<RP>& sm) {
 #pragma unroll
       for (int c = 0; c < NCT; ++c) acc[c] = mfma32(a, qv[c][kp], acc[c]);
     }
-#pragma unroll
-    for (int c = 0; c < NCT; ++c) {
-      const int col = cw + 32 * c + li;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = row0 + mf32_row(v, g);
-        if (row < r_hi && col < d.n) {
-          const float mh = acc[c][v];
-          const int64_t pr = prow<RM>(d, row);
-          if (WM) store_mhat_nt<OUTBF>(d, pr * d.ldh + col, mh);
-          if (WE) {
-            const float e = rawa_val<DT, SA, 1>(av[c][v], 0) - mh;
-            __builtin_nontemporal_store(e, RM ? d.err_fin + pr * d.lde_fin + col
-                                              : d.err_out + pr * d.lde_out + col);
-          }
-        }
-      }
-    }
+    if constexpr (EPI) lm_epi_store<NCT, WM, WE, OUTBF, RM>(d, vec, row0, r_hi, cw, acc, a4, sm.ep[wave]);
+    else lm_direct_store<NCT, WM, WE, OUTBF, RM>(d, row0, r_hi, cw, acc, av);
     if (more) {
       if (SRC == 0) {
 #pragma unroll
@@ -1839,7 +1959,7 @@ __global__ __launch_bounds__(kBlock) void k_ml(OCC_KARGS) {
 //   B operand  Q^T: lane (g, li) supplies the same ranks of its column
 //              cw + 32 c + li, split once into bf16 hi/lo registers;
 // so acc[c][v] = M_hat[row0 + mf32_row(v, g)][cw + 32 c + li], the layout of
-// k_ml, and err = A - M_hat is formed and stored as there.  Rounding both
+// k_ml, and err = A - M_hat is formed and stored straight from it.  Rounding both
 // factors to two bf16 parts leaves about 2^-16 of |M_hat| per element, far
 // inside bf16 input precision; at rank 128 the pass needs 3/16 of the
 // matrix-core cycles of the fp32 form and is bound by memory instead.
@@ -1937,14 +2057,8 @@ __device__ __forceinline__ void lmx_body(const Desc& d, int b, LMXSmem<RP>& sm) 
     const bool more = tile + 1 < ntile;
     if (more) lmx_fetch<RP, SRC>(d, row0 + 32, pr);
     // A for this tile's outputs (issued before the products to hide latency)
-    RawA<DT_F32, SA_SAVED, 1> av[NCT][16];
-    if (WE) {
-#pragma unroll
-      for (int c = 0; c < NCT; ++c)
-#pragma unroll
-        for (int v = 0; v < 16; ++v)
-          av[c][v] = rawa_load<DT_F32, SA_SAVED, 1, RM>(d, true, row0 + mf32_row(v, g), cw + 32 * c + li, d.n);
-    }
+    float av[NCT][16];
+    if (WE) lm_direct_load<NCT>(d, row0, cw, av);
     f16v acc[NCT];
 #pragma unroll
     for (int c = 0; c < NCT; ++c) acc[c] = f16v{};
@@ -1961,24 +2075,7 @@ __device__ __forceinline__ void lmx_body(const Desc& d, int b, LMXSmem<RP>& sm) 
         acc[c] = mfma32bf(al, bh[c][s2], acc[c]);
       }
     }
-#pragma unroll
-    for (int c = 0; c < NCT; ++c) {
-      const int col = cw + 32 * c + li;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = row0 + mf32_row(v, g);
-        if (row < r_hi && col < d.n) {
-          const float mh = acc[c][v];
-          const int64_t pr = prow<RM>(d, row);
-          if (WM) store_mhat_nt<OUTBF>(d, pr * d.ldh + col, mh);
-          if (WE) {
-            const float e = rawa_val<DT_F32, SA_SAVED, 1>(av[c][v], 0) - mh;
-            __builtin_nontemporal_store(e, RM ? d.err_fin + pr * d.lde_fin + col
-                                              : d.err_out + pr * d.lde_out + col);
-          }
-        }
-      }
-    }
+    lm_direct_store<NCT, WM, WE, OUTBF, RM>(d, row0, r_hi, cw, acc, av);
     if (more) lmx_stage<RP>(pr, sm.p[(tile + 1) & 1]);
     __syncthreads();
   }

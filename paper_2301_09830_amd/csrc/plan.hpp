@@ -134,6 +134,11 @@ __host__ __device__ constexpr int lq_block_cols(int rp) { return 128 * lq_cpl(rp
 // reconstruction: 32-column MFMA tiles per wave and columns per block
 __host__ __device__ constexpr int lm_tiles(int rp) { return rp >= 64 ? 1 : 2; }
 __host__ __device__ constexpr int lm_block_cols(int rp) { return 128 * lm_tiles(rp); }
+// reconstruction of fp32 M (k_ml): outputs through an LDS tile and stored by
+// rows with 16-byte accesses at padded rank 64 (51200 x 3072: 393 -> 369 us);
+// at rank 32 (two 32-column tiles per wave) stored straight from the MFMA
+// layout, which measured faster there (2.50 vs 2.81 ms on 36 stage matrices)
+__host__ __device__ constexpr bool lm_lds_epilogue(int rp) { return rp == 64; }
 
 // Blocks of each large-rank streaming kernel that are resident on the
 // device at once (compute units x blocks per compute unit).  Grids are
