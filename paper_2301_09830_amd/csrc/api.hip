@@ -185,7 +185,7 @@ Slots device_slots_for(int dev) {
                  0) == hipSuccess;
   if constexpr (X3)
     ok = ok && hipOccupancyMaxActiveBlocksPerMultiprocessor(&bq, k_lqx<DT_F32, RP, SA_SAVED, true>,
-                                                            kBlock, 0) == hipSuccess;
+                                                            lqx_waves(RP) * kWave, 0) == hipSuccess;
   else
     ok = ok && hipOccupancyMaxActiveBlocksPerMultiprocessor(&bq, k_lq<DT_F32, RP, SA_SAVED, true>,
                                                             kBlock, 0) == hipSuccess;
@@ -479,12 +479,13 @@ occ_status_t run_batch_t(const Batch& b, void* ws, uint32_t* flags, bool finish,
           L("apply2", k_lapply<RP, 1>, b.blocks[K_APPLY]);
           if constexpr (X3) {
             // the stored A through LDS tiles under the same conditions
+            constexpr int QXT = lqx_waves(RP) * kWave;
             if (saved && whole)
-              L("pass_q_a", k_lqx<DT_F32, RP, SA_SAVED, TL>, b.blocks[K_PASS_Q]);
+              LB("pass_q_a", k_lqx<DT_F32, RP, SA_SAVED, TL>, b.blocks[K_PASS_Q], QXT);
             else if (saved)
-              L("pass_q_a", k_lqx<DT_F32, RP, SA_SAVED, false>, b.blocks[K_PASS_Q]);
+              LB("pass_q_a", k_lqx<DT_F32, RP, SA_SAVED, false>, b.blocks[K_PASS_Q], QXT);
             else
-              L("pass_q", k_lqx<DT, RP, SA_MERR, false, RM>, b.blocks[K_PASS_Q]);
+              LB("pass_q", k_lqx<DT, RP, SA_MERR, false, RM>, b.blocks[K_PASS_Q], QXT);
           } else {
             if (saved && whole)
               L("pass_q_a", k_lq<DT_F32, RP, SA_SAVED, TL>, b.blocks[K_PASS_Q]);

@@ -1428,15 +1428,17 @@ __device__ __forceinline__ int lqx_slot(int li, int g) { return 2 * li + (g ^ ((
 // Slots are 1152 bytes apart, so at CPL = 1 (one 128-byte row per half-wave
 // of an operand read) rows e and 8 + e fall in opposite halves of the banks.
 constexpr int LQX_SLOT = 1024 + 128;
+#ifndef LQX_AST
+#define LQX_AST 3
+#endif
 template <int RP>
 struct LQXTile {
   static constexpr int CPL = lq_cpl(RP);
   static constexpr int RPI = 8 / CPL;                 // rows per load instruction
   static constexpr int NI = LQX_G / RPI;              // slots per group
   static constexpr int BYTES = NI * LQX_SLOT;         // one stage of one wave
-  // stages per wave: at rank 128 the A tiles run three groups ahead (with
-  // the P tile's two stages, three blocks fit a compute unit's LDS)
-  static constexpr int AST = RP >= 128 ? 4 : 2;
+  // stages per wave: at rank 128 the A tiles run LQX_AST - 1 groups ahead
+  static constexpr int AST = RP >= 128 ? LQX_AST : 2;
 };
 
 // Rows r0 .. r0+15 (clamped to r_last) of columns cw .. cw + 32 CPL - 1
@@ -1474,7 +1476,8 @@ __device__ __forceinline__ void lqx_tile_read(const uint8_t* src, int li, int g,
 template <int DT, int RP, int SA, bool TILES, bool RM = false>
 __device__ __forceinline__ void lqx_body(const Desc& d, int b, LQXSmem<RP>& sm, uint8_t* tiles) {
   static_assert(!(TILES && RM), "the row map runs on the register form");
-  constexpr int NU = RP / 32, CPL = lq_cpl(RP), BC = lq_block_cols(RP);
+  constexpr int NU = RP / 32, CPL = lq_cpl(RP), BC = lq_block_cols(RP, true);
+  constexpr int NW = lqx_waves(RP);
   constexpr int NLD = 2 * NU;                         // P tile load instructions per group
   const bool vec = d.vec != 0;
   const int wave = wave_id(), lane = threadIdx.x & 63;
@@ -1499,7 +1502,7 @@ __device__ __forceinline__ void lqx_body(const Desc& d, int b, LQXSmem<RP>& sm, 
     const int r0 = r_lo + LQX_G * grp;   // a multiple of 16
     const int rk = lane >> 1, h = (lane & 1) ^ ((lane >> 4) & 1);
 #pragma unroll
-    for (int j = wave; j < NLD; j += kBlock / kWave) {
+    for (int j = wave; j < NLD; j += NW) {
       const int part = j / NU, u = j % NU;
       const uint16_t* src = ptb + (((int64_t)(r0 >> 4) * 2 + part) * RP + 32 * u + rk) * 16 + 8 * h;
       __builtin_amdgcn_global_load_lds((gvoid_t*)src, (lvoid_t*)(&sm.p[stage][part][32 * u * LQX_G]),
@@ -1679,16 +1682,15 @@ __device__ __forceinline__ void lqx_body(const Desc& d, int b, LQXSmem<RP>& sm, 
 }
 
 template <int DT, int RP, int SA, bool TILES, bool RM = false>
-__global__ __launch_bounds__(kBlock) void k_lqx(OCC_KARGS) {
+__global__ __launch_bounds__(lqx_waves(RP) * kWave) void k_lqx(OCC_KARGS) {
   __shared__ __attribute__((aligned(16))) LQXSmem<RP> sm;
-  __shared__ __attribute__((aligned(16))) uint8_t tiles[TILES ? 4 * LQXTile<RP>::AST * LQXTile<RP>::BYTES : 16];
+  __shared__ __attribute__((aligned(16)))
+  uint8_t tiles[TILES ? lqx_waves(RP) * LQXTile<RP>::AST * LQXTile<RP>::BYTES : 16];
 #define B_(d, b) lqx_body<DT, RP, SA, TILES, RM>(d, b, sm, tiles)
   OCC_DISPATCH_X(K_PASS_Q, B_)
 #undef B_
 }
 
-// One element of M_hat, nontemporal: fp32, or bf16 (round to nearest even)
-// when OUTBF (stand-alone decompression only).
 // -------------------------------------------------------------------------
 // Epilogue of the reconstruction passes (k_ml, k_mlx).  The products leave
 // each 32 x 32 tile of M_hat in the 32x32 MFMA layout: lane (g, li) holds

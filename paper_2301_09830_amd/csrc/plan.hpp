@@ -130,7 +130,13 @@ constexpr int64_t L_MIN_ROWS = 1024;      // right product: rows per split, at l
 constexpr int64_t L_MIN_NARROW = 256;     // the same for matrices that cannot fill a round
 // right product: columns per lane and per block
 __host__ __device__ constexpr int lq_cpl(int rp) { return rp >= 128 ? 1 : 128 / rp; }
-__host__ __device__ constexpr int lq_block_cols(int rp) { return 128 * lq_cpl(rp); }
+// waves per block of the split bf16 right product (k_lqx): 8 at padded rank
+// 128, so that a block's P_hat^T tile of each 16-row group (as many bytes
+// as 128 columns of A) serves 256 columns
+__host__ __device__ constexpr int lqx_waves(int rp) { return rp >= 128 ? 8 : 4; }
+__host__ __device__ constexpr int lq_block_cols(int rp, bool x3 = false) {
+  return (x3 ? 32 * lqx_waves(rp) : 128) * lq_cpl(rp);
+}
 // reconstruction: 32-column MFMA tiles per wave and columns per block
 __host__ __device__ constexpr int lm_tiles(int rp) { return rp >= 64 ? 1 : 2; }
 __host__ __device__ constexpr int lm_block_cols(int rp) { return 128 * lm_tiles(rp); }
@@ -222,7 +228,7 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0,
   t.grows = (int)clamp64(round_up(cdiv(m, g_want), 32), 32, L_GROWS);
   t.ng = (int)cdiv(m, t.grows);
   // right product: column tiles, rows split
-  const int64_t ctq = cdiv(n, lq_block_cols(rp));
+  const int64_t ctq = cdiv(n, lq_block_cols(rp, x3));
   // splits of L_MIN_ROWS rows, halved (down to L_MIN_NARROW) while they
   // would leave this matrix's share of one round of resident blocks partly
   // empty (a single 51200 x 3072 matrix at rank 64: 600 of 1024 slots, so

@@ -253,21 +253,24 @@ def loop_waits(body):
 
 def wait_violations(funcs):
     """(kernels checked, problems).  Stage loops wait for {0, c, 2c}; the bf16
-    rank-RP right product for c minus its P-tile share ceil(2 (RP / 32) / 4)."""
+    rank-RP right product for c minus its P-tile share ceil(2 (RP / 32) / W),
+    W its waves per block (8 at rank 128, else 4)."""
     checked, bad = set(), []
     for name, body in funcs.items():
         for waits, c in loop_waits(body):
             checked.add(name)
             if "k_lqx" in name:
                 rp = int(re.search(r"k_lqxILi\d+ELi(\d+)E", name).group(1))
-                share = -(-2 * (rp // 32) // 4)
+                share = -(-2 * (rp // 32) // (8 if rp >= 128 else 4))
                 want = [0, c - share]
             elif "k_pm" in name or "k_lq" in name:
                 want = [0, c, 2 * c]
             else:
                 bad.append((name, "unknown loop with hand-written vmcnt waits", waits, c))
                 continue
-            if waits != want or c <= 0 or want[1] <= 0:
+            # a loop may hold only some of them (the compiler peels or
+            # versions the stage loop), never another value
+            if not set(waits) <= set(want) or c <= 0 or want[1] <= 0:
                 bad.append((name, waits, c, want))
     return checked, bad
 
