@@ -1428,9 +1428,9 @@ __device__ __forceinline__ int lqx_slot(int li, int g) { return 2 * li + (g ^ ((
 // Slots are 1152 bytes apart, so at CPL = 1 (one 128-byte row per half-wave
 // of an operand read) rows e and 8 + e fall in opposite halves of the banks.
 constexpr int LQX_SLOT = 1024 + 128;
-#ifndef LQX_AST
-#define LQX_AST 3
-#endif
+// stages of A per wave at rank 128 (two groups ahead; two 8-wave blocks per
+// compute unit)
+constexpr int LQX_AST = 3;
 template <int RP>
 struct LQXTile {
   static constexpr int CPL = lq_cpl(RP);
