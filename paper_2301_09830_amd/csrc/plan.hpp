@@ -207,7 +207,10 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0,
     return std::max<int64_t>(std::max<int64_t>(1, total / 4), (int64_t)(share * (double)total + 0.5));
   };
   const int64_t target = target_of(L_SPLIT_BLOCKS, sl.p);
-  const int64_t target_q = target_of(L_SPLIT_BLOCKS, sl.q);
+  // the bf16 rank-128 right product (two 8-wave blocks per compute unit)
+  // aims at half as many blocks: one round, half the row splits, so half
+  // the partials for the Q reduction (4 x 16384 x 8192: 4.16 -> 4.12 ms)
+  const int64_t target_q = target_of(x3 && rp >= 128 ? L_SPLIT_BLOCKS / 2 : L_SPLIT_BLOCKS, sl.q);
   const int64_t target_m = target_of(2 * L_SPLIT_BLOCKS, sl.m);
   // left product: 128-row tiles, columns split, splits at least L_MIN_COLS
   // wide -- narrower, down to L_MIN_NARROW, while this matrix's blocks would
