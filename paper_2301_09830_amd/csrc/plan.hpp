@@ -206,7 +206,10 @@ inline Tiling make_tiling(int64_t m, int64_t n, int rp, double share = 1.0,
     const int64_t total = whole_rounds(want, slots);
     return std::max<int64_t>(std::max<int64_t>(1, total / 4), (int64_t)(share * (double)total + 0.5));
   };
-  const int64_t target = target_of(L_SPLIT_BLOCKS, sl.p);
+  // the bf16 rank-128 left product (one 8-wave block per compute unit) aims
+  // at half as many blocks: half the column splits, so half the P partials
+  // written and summed (4 x 16384 x 8192: 4.11 -> 4.07 ms; a quarter: 4.10)
+  const int64_t target = target_of(x3 && rp >= 128 ? L_SPLIT_BLOCKS / 2 : L_SPLIT_BLOCKS, sl.p);
   // the bf16 rank-128 right product (two 8-wave blocks per compute unit)
   // aims at half as many blocks: one round, half the row splits, so half
   // the partials for the Q reduction (4 x 16384 x 8192: 4.16 -> 4.12 ms)
