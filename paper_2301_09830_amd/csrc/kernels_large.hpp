@@ -1044,15 +1044,28 @@ __device__ __forceinline__ void la_body(const Desc& d, int b, LASmem<RP>& sm) {
   for (int s = 0; s < KB_MAX; ++s) tb[s] = (s < kb) ? Tg[(4 * s + q) * RP + 16 * jb + li] : 0.0;
 
   const int r_lo = b * L_AROWS, r_hi = min(d.m, r_lo + L_AROWS);
+  // the rows of S of the next chunk are loaded into registers while this
+  // chunk's products and stores run (rows past m as zeros)
+  constexpr int SF = CR * RP / 4 / kBlock;   // float4s per thread per chunk
+  static_assert(SF * kBlock == CR * RP / 4, "chunk staging layout");
+  float4 nx[SF];
+  auto fetch = [&](int c0) {
+#pragma unroll
+    for (int x = 0; x < SF; ++x) {
+      const int idx = t + kBlock * x, i = idx / (RP / 4), k4 = idx % (RP / 4);
+      nx[x] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (c0 + i < r_hi) nx[x] = *(const float4*)(src + (int64_t)(c0 + i) * RP + 4 * k4);
+    }
+  };
+  if (r_lo < r_hi) fetch(r_lo);
   for (int c0 = r_lo; c0 < r_hi; c0 += CR) {
-    // stage the chunk's rows of S (rows past m as zeros)
-    for (int idx = t; idx < CR * RP / 4; idx += kBlock) {
-      const int i = idx / (RP / 4), k4 = idx % (RP / 4);
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (c0 + i < r_hi) v = *(const float4*)(src + (int64_t)(c0 + i) * RP + 4 * k4);
-      *(float4*)&sm.buf[i][4 * k4] = v;
+#pragma unroll
+    for (int x = 0; x < SF; ++x) {
+      const int idx = t + kBlock * x, i = idx / (RP / 4), k4 = idx % (RP / 4);
+      *(float4*)&sm.buf[i][4 * k4] = nx[x];
     }
     __syncthreads();
+    if (c0 + CR < r_hi) fetch(c0 + CR);
     d4v acc[2][2];
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
