@@ -211,6 +211,28 @@ def test_unaligned_leading_dimension():
     assert_parity(res, "bf16", "bf16 ld = n + 3 (scalar path)")
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("ld_pad", [1, 2])
+@pytest.mark.parametrize("rank", [32, 64, 128])
+def test_large_rank_padded_rows(rank, ld_pad, dtype):
+    """Rows of pitch n + 1 (a multiple of 4: 16-byte accesses, with a ragged
+    last piece of 3 columns) and n + 2 (element accesses) at padded ranks
+    32-128, where the reconstruction stores straight from the MFMA layout
+    (rank 32, 128, bf16) or through an LDS tile by rows (fp32 rank 64).  The
+    padding columns of err and M_hat must never be written."""
+    shape = (300, 151)
+    if dtype == "f32":
+        w = Workload(95, "ldpad_large", (shape,), "f32", rank, 2, 2, "gauss", std=1.0)
+    else:
+        w = WORKLOADS[5].scaled([shape], rank=rank)
+    res, states, _ = run_workload(w, 2, ld_pad=ld_pad)
+    assert_parity(res, dtype, f"{dtype} {shape} rank {rank} ld = n + {ld_pad}")
+    torch = torch_mod()
+    st = states[0]
+    assert bool(torch.isnan(st.Mh_full[:, shape[1]:]).all()), "M_hat padding written"
+    assert bool((st.err_full[:, shape[1]:] == 0).all()), "err padding written"
+
+
 @pytest.mark.parametrize("snr", [False, True])
 @pytest.mark.parametrize("rank", [32, 64, 128])
 def test_bf16_large_rank_split_products_accuracy(rank, snr):
