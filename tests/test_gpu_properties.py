@@ -48,7 +48,7 @@ def test_invariants_fp32_level(rank):
     assert ortho <= 1e-4 * err.double().norm().item()
 
 
-@pytest.mark.parametrize("rank,dtype", [(12, "bf16"), (40, "bf16"), (100, "f32")])
+@pytest.mark.parametrize("rank,dtype", [(12, "bf16"), (40, "bf16"), (64, "f32"), (100, "f32")])
 def test_fused_equals_unfused_bitwise(rank, dtype):
     """occ_step (large ranks: A stored over err, later passes read it back)
     equals occ_compress (re-reads M + err_prev) + occ_decompress +
@@ -287,7 +287,8 @@ def test_nonfinite_input_propagates_and_flags(rank):
 
 
 @pytest.mark.parametrize("split", [False, True])
-@pytest.mark.parametrize("rank,pad", [(4, 0), (16, 0), (16, 3), (40, 0), (128, 0), (128, 5)])
+@pytest.mark.parametrize("rank,pad", [(4, 0), (16, 0), (16, 3), (40, 0), (40, 3), (64, 0), (128, 0),
+                                      (128, 5)])
 def test_decompress_bf16_output_is_rne_of_fp32(rank, pad, split):
     """OCC_DEC_OUT_BF16 stores every element of M_hat rounded to nearest even
     from the fp32 value the same call computes without it: bitwise equal to
